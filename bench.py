@@ -1,0 +1,271 @@
+#!/usr/bin/env python3
+"""Benchmark of the tree-verification step on one MI355X.
+
+A step = one Llama-3-70B-shaped decoder layer verifying a 32-token draft
+tree (8 levels, branching <= 4) over a 4096-token prefix (int4 group-128
+weights, fp16 activations and KV cache), followed by the KV commit of the
+accepted path; the whole step is one replayed HIP graph.  Inputs are seeded
+synthetic tensors already resident in HBM.  Several copies of the layer
+(weights and KV cache) are rotated so the 256 MB Infinity Cache cannot hold
+the working set.
+
+Prints one JSON line: value = microseconds per layer-step (lower is better),
+plus the roofline of the dominant kernel (the fused SwiGLU W4A16 GEMM) timed
+on its own stream with HIP events, and the fp64 CPU reference checker timed
+on the host as a baseline.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c3")
+    ap.add_argument("--copies", type=int, default=0, help="layer copies rotated (0: auto)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only-kernel", default="", help="launch only this kernel (for counter runs): "
+                    "swiglu | qkv | o | down | attention | commit | copy")
+    ap.add_argument("--iters", type=int, default=50)
+    return ap.parse_args()
+
+
+def source_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+GEMM_SOURCES = ["paper_2506_11309_amd/csrc/w4a16_gemm.hip", "paper_2506_11309_amd/csrc/ss_device.h"]
+
+
+def read_traffic(kernel_tag, cur_hash):
+    """HBM bytes per launch measured by rocprofv3 counters (committed summary),
+    or None if absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != cur_hash:
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU path "
+              "is not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2506_11309_amd as ss
+    from gen import workloads as wl
+
+    if not os.path.exists(ss.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = wl.CONFIGS[args.config]
+    s = cfg.shape
+    T = cfg.T
+
+    t0 = time.time()
+    w = wl.make_layer_weights(cfg)
+    kc, vc = wl.make_kv_prefix(cfg)
+    x = wl.make_activations(cfg)
+    parent, acc = wl.make_tree(cfg)
+    gen_s = time.time() - t0
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            a = a.view(np.int16)
+        return torch.from_numpy(a).to(dev)
+
+    layer_bytes = s.w4_bytes() + cfg.kv_bytes_per_layer()
+    copies = args.copies or max(2, -(-2 * MALL_BYTES // layer_bytes) + 1)
+    stream = torch.cuda.Stream()
+    dims = ss.make_dims(s.H, s.Hq, s.Hkv, s.D, s.F, cfg.S_max)
+    rope = up(ss.rope_table(500000.0, cfg.S_max, s.D))
+    dparent = up(parent)
+    dacc = up(np.array([acc], np.int32))
+    host_w = {n: (w[n]["qweight"], w[n]["scales"], w[n]["zeros"]) for n in ("wqkv", "wo", "wgate", "wup", "wdown")}
+    inst = []
+    for c in range(copies):
+        keep = {n: tuple(up(a) for a in host_w[n]) for n in host_w}
+        w4 = {n: ss.make_w4(*keep[n]) for n in keep}
+        d = {"keep": keep, "w4": w4, "an": up(w["attn_norm"]), "mn": up(w["mlp_norm"]),
+             "kc": up(kc), "vc": up(vc), "P": up(np.array([cfg.P], np.int32)), "h": up(x)}
+        d["layer"] = ss.make_layer(d["an"], d["mn"], w4["wqkv"], w4["wo"], w4["wgate"], w4["wup"],
+                                   w4["wdown"], d["kc"], d["vc"])
+        d["ws"] = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
+        inst.append(d)
+    torch.cuda.synchronize()
+
+    # ---------------- counter-run mode: one kernel type only ----------------
+    if args.only_kernel:
+        run_only(args, ss, torch, np, inst, cfg, dims, dparent, dacc, rope, stream, dev)
+        return
+
+    # ---------------- step graphs ----------------
+    graphs = []
+    with torch.cuda.stream(stream):
+        for d in inst:
+            g = ss.Graph()
+            g.begin(stream)
+            ss.verify_layer(d["layer"], dims, d["h"], d["P"], dparent, rope, d["ws"], stream=stream)
+            ss.kv_commit(d["kc"], d["vc"], d["P"], dparent, dacc, advance=False, ws=d["ws"], stream=stream)
+            g.end(stream)
+            graphs.append(g)
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            graphs[i % copies].launch(stream)
+    stream.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        start.record(stream)
+        for i in range(args.steps):
+            graphs[i % copies].launch(stream)
+        stop.record(stream)
+    stop.synchronize()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    for d in inst:
+        err = ss.read_device_error(d["ws"], stream)
+        if err:
+            raise RuntimeError(f"device error word {err}")
+
+    # ---------------- dominant kernel: fused SwiGLU GEMM ----------------
+    m_buf = torch.zeros((T, s.F), dtype=torch.int16, device=dev)
+    xin = up(x)
+    sw_ws = ss.workspace(ss.swiglu_workspace_bytes(T, s.H, s.F), dev)
+    sw_iters = max(args.steps, 50)
+    with torch.cuda.stream(stream):
+        for i in range(5):
+            d = inst[i % copies]
+            ss.w4a16_swiglu(d["w4"]["wgate"], d["w4"]["wup"], xin, m_buf, sw_ws, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(sw_iters):
+            d = inst[i % copies]
+            ss.w4a16_swiglu(d["w4"]["wgate"], d["w4"]["wup"], xin, m_buf, sw_ws, stream=stream)
+        e1.record(stream)
+    e1.synchronize()
+    sw_us = e0.elapsed_time(e1) * 1000.0 / sw_iters
+    sw_bytes = 2 * (s.H * s.F // 2 + (s.H // 128) * s.F * 3)
+    sw_gbs = sw_bytes / (sw_us * 1e-6) / 1e9
+    traffic = read_traffic("swiglu_gemm_c3", source_hash(GEMM_SOURCES))
+
+    # ---------------- CPU baseline: the fp64 reference checker ----------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        odims = {"H": s.H, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "F": s.F, "S_max": cfg.S_max}
+        okc, ovc = kc.copy(), vc.copy()
+        t1 = time.time()
+        oracle.verify_layer(odims, w, okc, ovc, x, cfg.P, parent)
+        oracle.kv_commit(okc, ovc, cfg.P, parent, acc)
+        cpu_s = time.time() - t1
+        cpu = {"value": round(cpu_s * 1e6, 1), "unit": "us/layer", "cores": oracle.num_threads(),
+               "kind": "oracle",
+               "sample": f"one full {cfg.name} layer step (T={T}, P={cfg.P}) + commit, fp64, "
+                         f"{oracle.num_threads()} OpenMP threads, timed once"}
+
+    step_bytes = s.w4_bytes() + cfg.kv_bytes_per_layer()
+    out = {
+        "metric": "tree-verify step latency (us/layer) + achieved HBM GB/s vs peak, 1 MI355X",
+        "value": round(ms_step * 1000.0, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 (int4 weights, fp32 accumulate)",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: Llama-3-70B-shaped layer, H={s.H}, Hq/Hkv={s.Hq}/{s.Hkv}, "
+                               f"D={s.D}, F={s.F}, int4 g128; tree T={T} ({cfg.levels} levels, "
+                               f"branching<={cfg.branching}); prefix P={cfg.P}; verify + KV commit",
+                   "global_batch": T, "seq_len": cfg.P + T, "parallelism": "none (1 GPU)",
+                   "layer_copies_rotated": copies},
+        "step_hbm_gbs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "roofline": {"kernel": "w4a16_swiglu (gate+up, fused)", "bound": "hbm",
+                     "achieved": round(sw_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(sw_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": sw_bytes, "avg_launch_us": round(sw_us, 3)},
+        "cpu_baseline": cpu,
+        "input_generation_s": round(gen_s, 2),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_only(args, ss, torch, np, inst, cfg, dims, dparent, dacc, rope, stream, dev):
+    """Launch a single kernel type `iters` times (rotating layer copies) for
+    rocprofv3 counter collection; prints what it ran."""
+    s = cfg.shape
+    T = cfg.T
+    copies = len(inst)
+    kind = args.only_kernel
+    xin = torch.zeros((T, max(s.H, s.F)), dtype=torch.int16, device=dev)
+    xin.copy_(torch.randint(-3000, 3000, xin.shape, dtype=torch.int16, device=dev) & 0x3BFF)
+    out = torch.zeros((T, max(s.F, s.n_qkv)), dtype=torch.int16, device=dev)
+    ws = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
+    qkv = torch.zeros((T, s.n_qkv), dtype=torch.int16, device=dev)
+    big = torch.zeros(256 << 20, dtype=torch.uint8, device=dev)
+    big2 = torch.empty_like(big)
+    with torch.cuda.stream(stream):
+        for i in range(args.iters):
+            d = inst[i % copies]
+            if kind == "swiglu":
+                ss.w4a16_swiglu(d["w4"]["wgate"], d["w4"]["wup"], xin[:, :s.H], out[:, :s.F], ws, stream=stream)
+            elif kind == "qkv":
+                ss.w4a16_gemm(d["w4"]["wqkv"], xin[:, :s.H], out[:, :s.n_qkv], ws, stream=stream)
+            elif kind == "o":
+                ss.w4a16_gemm(d["w4"]["wo"], xin[:, :s.Hq * s.D], out[:, :s.H], ws, stream=stream)
+            elif kind == "down":
+                ss.w4a16_gemm(d["w4"]["wdown"], xin[:, :s.F], out[:, :s.H], ws, stream=stream)
+            elif kind == "attention":
+                Hd = s.Hq * s.D
+                ss.tree_attention(qkv, qkv[:, Hd:], qkv[:, Hd + s.Hkv * s.D:], d["kc"], d["vc"], d["P"], dparent,
+                                  s.Hq, s.Hkv, s.D, rope, out[:, :Hd], ws, stream=stream)
+            elif kind == "commit":
+                ss.kv_commit(d["kc"], d["vc"], d["P"], dparent, dacc, ws=ws, stream=stream)
+            elif kind == "copy":
+                big2.copy_(big)
+            else:
+                raise SystemExit(f"unknown kernel {kind}")
+    stream.synchronize()
+    print(json.dumps({"only_kernel": kind, "iters": args.iters, "copies": copies,
+                      "copy_bytes": big.numel() if kind == "copy" else None}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,242 @@
+/*
+ * swiftspec -- tree-verification forward step for speculative decoding on
+ * AMD Instinct MI355X (gfx950).  C ABI of libswiftspec.so.
+ *
+ * The operations follow SwiftSpec (arXiv 2506.11309):
+ *   - the target model verifies a draft token tree by one batched forward
+ *     pass (Algorithm 1, target-worker branch; Sec. 3.1);
+ *   - inside the tree a token attends only to itself and its ancestors, and
+ *     to the whole verified prefix (Sec. 3.1, paragraph on non-square masks,
+ *     square mask of the target model);
+ *   - rotary position embedding is fused into attention, a token's position
+ *     being prefix length + its depth in the tree (Sec. 3.3, masked
+ *     attention; Sec. 4, tree bookkeeping by depth and ancestor list);
+ *   - weights are int4 AWQ-style with group size 128, compute is 16-bit
+ *     (Sec. 5.1);
+ *   - the MLP is a fused SwiGLU (Sec. 3.3, fused SwiGLU);
+ *   - after verification the KV states of the verified tokens are kept as a
+ *     contiguous prefix of the cache, the tree region following it
+ *     (Sec. 3.2 and the caption of Fig. 5); the verified path begins at the
+ *     current tree root (Sec. 3.1, walk-through of Fig. 3).
+ *
+ * Conventions
+ *   - fp16 tensors are passed as uint16_t IEEE binary16 bit patterns.
+ *   - Unless stated otherwise every tensor pointer is DEVICE memory owned by
+ *     the caller (e.g. allocated by PyTorch).  The library never allocates
+ *     device memory and never frees caller memory.
+ *   - Row-major layouts; leading dimensions (ld*) are in elements.  Device
+ *     tensors and leading dimensions must keep 16-byte alignment of every
+ *     row (ld % 8 == 0 for fp16) unless stated otherwise.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
+ *     the null stream).  No call synchronises the stream or reads device
+ *     data on the host, so every compute call can be captured into a HIP
+ *     graph.  Host-side argument checks happen before any launch; on error
+ *     nothing is launched.
+ *   - Scratch memory is a caller-provided device workspace whose size comes
+ *     from the matching *_workspace_bytes query.  The first
+ *     SWIFTSPEC_WS_HEADER_BYTES bytes of every workspace hold an error word
+ *     and ticket counters that must be zero before first use (allocate it
+ *     zero-filled or call swiftspec_workspace_init once); every call leaves
+ *     them zero again.  Calls sharing one workspace must not overlap in
+ *     time (use one stream per workspace).
+ *   - Per-step data that lives in device memory (prefix length, parent
+ *     array, accepted node) is validated on the device: an invalid value
+ *     sets a bit of the workspace error word (swiftspec_read_device_error)
+ *     and the affected kernels skip their writes; they never access memory
+ *     out of bounds.
+ *   - Thread safety: calls are stateless apart from a thread-local record of
+ *     the last HIP error.
+ */
+#ifndef SWIFTSPEC_H
+#define SWIFTSPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+enum {
+  SWIFTSPEC_OK = 0,
+  SWIFTSPEC_INVALID_ARG = 1,         /* null pointer, bad dimension, bad leading dimension */
+  SWIFTSPEC_UNSUPPORTED = 2,         /* D not 64/128, T > 64, K % 128, M > 64, Hq % Hkv ... */
+  SWIFTSPEC_MISALIGNED = 3,          /* pointer or leading dimension breaks 16-byte alignment */
+  SWIFTSPEC_WORKSPACE_TOO_SMALL = 4, /* ws_bytes below the *_workspace_bytes figure */
+  SWIFTSPEC_BAD_TREE = 5,            /* host-side tree validation failed */
+  SWIFTSPEC_HIP_ERROR = 6            /* a HIP runtime call failed; see swiftspec_last_hip_error */
+};
+
+/* bits of the device error word */
+#define SWIFTSPEC_DEVERR_BAD_TREE 1u     /* parent[0] != -1 or parent[i] outside [0, i) */
+#define SWIFTSPEC_DEVERR_BAD_PREFIX 2u   /* prefix length < 0 or prefix + T > S_max */
+#define SWIFTSPEC_DEVERR_BAD_ACCEPTED 4u /* accepted node outside [0, T) */
+
+#define SWIFTSPEC_WS_HEADER_BYTES 65536u
+#define SWIFTSPEC_MAX_TREE 64 /* one 64-lane wavefront builds the ancestor masks */
+#define SWIFTSPEC_MAX_M 64    /* GEMM rows (tree tokens) per call */
+
+const char* swiftspec_status_string(int status);
+/* hipError_t of the last failing HIP call on this thread (0 if none). */
+int swiftspec_last_hip_error(void);
+/* Zero the workspace header on `stream` (a fill kernel, no memset). */
+int swiftspec_workspace_init(void* ws, size_t ws_bytes, void* stream);
+/* Synchronise `stream`, copy the error word to *out (host), then clear it. */
+int swiftspec_read_device_error(void* ws, void* stream, uint32_t* out);
+
+/* ------------------------------------------------------- int4 weights
+ * AWQ-style int4 matrix W (N output rows x K inputs), group size 128
+ * (Sec. 5.1).  Dequantised value W'[n][k] = (q[n][k] - z[n][k/128]) * s[n][k/128].
+ *   qweight: [N][K/2] bytes, byte b of row n holds k = 2b (low nibble) and
+ *            k = 2b + 1 (high nibble), values 0..15;
+ *   scales : [N][K/128] fp16;
+ *   zeros  : [N][K/128] uint8, values 0..15.
+ * K % 128 == 0, N % 16 == 0. */
+typedef struct {
+  const uint8_t* qweight;
+  const uint16_t* scales;
+  const uint8_t* zeros;
+  int32_t K, N;
+} swiftspec_w4;
+
+/* y[m][n] = fp16( sum_k x[m][k] * W'[n][k] + residual[m][n] ), fp32
+ * accumulation, for m < M (1 <= M <= 64).  residual may be NULL; it may
+ * alias y only if ldr == ldy.  x [M][ldx], y [M][ldy], residual [M][ldr].
+ * The weight projections of a decoder layer at GEMM M = tree size
+ * (Sec. 3.3; QKV, O, down projections). */
+int swiftspec_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, int32_t ldx,
+                         uint16_t* y, int32_t ldy, const uint16_t* residual, int32_t ldr,
+                         void* ws, size_t ws_bytes, void* stream);
+size_t swiftspec_w4a16_gemm_workspace_bytes(int32_t M, int32_t K, int32_t N);
+
+/* Fused SwiGLU (Sec. 3.3): y[m][n] = fp16( silu(g) * u ), g = x.Wg'^T,
+ * u = x.Wu'^T (fp32), silu(g) = g / (1 + exp(-g)).  Wg and Wu share K, N. */
+int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* x,
+                           int32_t M, int32_t ldx, uint16_t* y, int32_t ldy, void* ws,
+                           size_t ws_bytes, void* stream);
+size_t swiftspec_w4a16_swiglu_workspace_bytes(int32_t M, int32_t K, int32_t N);
+
+/* out[m][:] = fp16( x[m][:] / sqrt(mean(x[m][:]^2) + eps) * gamma ), M rows of H. */
+int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, const uint16_t* gamma,
+                      float eps, uint16_t* out, int32_t ldo, void* stream);
+
+/* ------------------------------------------------------- tree attention
+ * Tree-masked grouped-query attention of the T draft tokens over the KV
+ * cache (Sec. 3.1 target-side square mask; Sec. 3.3 masked attention with
+ * the position embedding fused in).
+ *   q       : [T][ldq]  query heads h = 0..Hq-1 at columns [h*D, (h+1)*D), before RoPE
+ *   k, v    : [T][ldkv] kv heads at columns [g*D, (g+1)*D), k before RoPE
+ *   k_cache, v_cache : [Hkv][S_max][D]; rows [0, P) hold the verified prefix
+ *             (already rotated); rows [P, P+T) RECEIVE fp16(rope(k)) and v.
+ *   d_prefix_len : device int32, P
+ *   d_parent : device int32[T], parent[0] = -1, 0 <= parent[i] < i
+ *   rope_cos_sin : device fp32 [S_max][D/2][2] (cos, sin) of pos * theta^(-2d/D),
+ *             see swiftspec_rope_table; rotation pairs (d, d + D/2)
+ *   out     : [T][ldo] fp16, query head h at columns [h*D, (h+1)*D)
+ * Node i at position P + depth(i) attends to cache rows [0, P) and to the
+ * tree rows P + j of its ancestors-or-self j; query head h reads kv head
+ * h / (Hq / Hkv).  1 <= T <= 64, D in {64, 128}, Hq % Hkv == 0.  An invalid
+ * tree or prefix length sets the device error word; then out and the cache
+ * are left untouched. */
+int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                             int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
+                             const int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,
+                             int32_t Hq, int32_t Hkv, int32_t D, const float* rope_cos_sin,
+                             float softmax_scale, uint16_t* out, int32_t ldo, void* ws,
+                             size_t ws_bytes, void* stream);
+size_t swiftspec_tree_attention_workspace_bytes(int32_t T, int32_t Hq, int32_t Hkv, int32_t D,
+                                                int32_t S_max);
+
+/* Host helper: (cos, sin) table [S_max][D/2][2] of angle pos * theta^(-2d/D),
+ * evaluated in fp64 and rounded to fp32, into host memory. */
+int swiftspec_rope_table(double theta, int32_t S_max, int32_t D, float* host_out);
+
+/* Device ancestor masks: for each of n_trees parent arrays ([n_trees][T],
+ * device), anc[t][i] bit j set iff j is i or an ancestor of i; depth[t][i];
+ * status[t] = 0 (valid) or SWIFTSPEC_DEVERR_BAD_TREE (then anc = self bit,
+ * depth = 0).  The same wavefront routine the attention and commit kernels
+ * use.  T <= 64. */
+int swiftspec_tree_masks(const int32_t* d_parents, int32_t n_trees, int32_t T, uint64_t* d_anc,
+                         int32_t* d_depth, int32_t* d_status, void* stream);
+
+/* Host helper: validates a host parent array; fills depth_out (host, may be NULL). */
+int swiftspec_tree_validate(const int32_t* parent_host, int32_t T, int32_t* depth_out);
+
+/* ------------------------------------------------------------ KV commit
+ * Moves the KV states of the accepted path into the contiguous prefix
+ * (Sec. 3.2, Fig. 5 caption; target side).  With the accepted node a and its
+ * root-to-node path pi_0 = 0, ..., pi_{L-1} = a (L = depth(a) + 1), for every
+ * layer l < n_layers, for K and V and every kv head:
+ *     row P + i  <-  row P + pi_i   (i < L, all sources read before any write)
+ * rows [P+L, P+T) are left unchanged.  Layer l's caches start at
+ * k_cache + l * layer_stride_elems.  If advance != 0 the device prefix
+ * length becomes P + L after the copy (stream-ordered).  ws may be NULL
+ * (then device errors are not reported); otherwise its header receives the
+ * error word. */
+int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
+                        int64_t layer_stride_elems, int32_t Hkv, int32_t S_max, int32_t D,
+                        int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,
+                        const int32_t* d_accepted_node, int32_t advance, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/* -------------------------------------------------------- decoder layer */
+typedef struct {
+  int32_t H, Hq, Hkv, D, F, S_max;
+  float eps;        /* RMSNorm epsilon */
+  float rope_theta; /* informational; the table passed in defines the rotation */
+} swiftspec_dims;
+
+typedef struct {
+  const uint16_t* attn_norm; /* [H] fp16 */
+  const uint16_t* mlp_norm;  /* [H] fp16 */
+  swiftspec_w4 wqkv;         /* K = H, N = (Hq + 2 Hkv) D: rows [Q heads | K heads | V heads] */
+  swiftspec_w4 wo;           /* K = Hq D, N = H */
+  swiftspec_w4 wgate, wup;   /* K = H, N = F */
+  swiftspec_w4 wdown;        /* K = F, N = H */
+  uint16_t* k_cache;         /* [Hkv][S_max][D] */
+  uint16_t* v_cache;
+} swiftspec_layer;
+
+/* One Llama decoder layer over the draft tree (Algorithm 1, batch verify):
+ *   xn = rmsnorm(x, attn_norm); qkv = xn.Wqkv'^T; o = tree_attention(qkv)
+ *   h = x + o.Wo'^T; hn = rmsnorm(h, mlp_norm); m = silu(hn.Wg'^T) * (hn.Wu'^T)
+ *   out = h + m.Wd'^T
+ * with fp16 storage of xn, qkv, o, h, hn, m, out.  hidden [T][H] is read as
+ * x and overwritten with out.  The caches receive the tree's keys and values
+ * at rows [P, P+T).  softmax scale 1/sqrt(D). */
+int swiftspec_verify_layer(const swiftspec_layer* layer, const swiftspec_dims* dims,
+                           uint16_t* hidden, int32_t T, const int32_t* d_prefix_len,
+                           const int32_t* d_parent, const float* rope_cos_sin, void* ws,
+                           size_t ws_bytes, void* stream);
+size_t swiftspec_verify_layer_workspace_bytes(const swiftspec_dims* dims, int32_t T);
+/* Byte offsets, inside the verify_layer workspace, of the layer's fp16
+ * intermediates after a call: offsets[0..5] = xn [T][H], qkv [T][(Hq+2Hkv)D],
+ * o [T][Hq D], h [T][H], hn [T][H], m [T][F] (row-major, dense).  For
+ * inspection and stage-by-stage checking; the contents are valid until the
+ * next call that uses the workspace. */
+int swiftspec_verify_layer_workspace_layout(const swiftspec_dims* dims, int32_t T, size_t* offsets);
+
+/* Final RMSNorm and fp16 LM head: logits[m][v] = fp16( rmsnorm(h[m], gamma) . W[v] ),
+ * h [M][H], W [V][H] fp16 (dense), logits [M][V].  1 <= M <= 64, H % 128 == 0,
+ * V % 16 == 0. */
+int swiftspec_lm_head(const uint16_t* h, int32_t M, int32_t H, const uint16_t* gamma, float eps,
+                      const uint16_t* W, int32_t V, uint16_t* logits, void* ws, size_t ws_bytes,
+                      void* stream);
+size_t swiftspec_lm_head_workspace_bytes(int32_t M, int32_t H, int32_t V);
+
+/* ---------------------------------------------------------- HIP graphs
+ * Capture the calls issued on `stream` between begin and end into an
+ * executable graph (hipStreamBeginCapture / hipGraphInstantiate) and replay
+ * it with swiftspec_graph_launch.  Device-resident prefix length and parent
+ * array make one graph valid for every step of a generation. */
+typedef struct swiftspec_graph swiftspec_graph;
+int swiftspec_graph_begin(void* stream);
+int swiftspec_graph_end(void* stream, swiftspec_graph** out);
+int swiftspec_graph_launch(swiftspec_graph* g, void* stream);
+int swiftspec_graph_destroy(swiftspec_graph* g);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

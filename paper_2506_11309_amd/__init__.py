@@ -1,0 +1,307 @@
+"""Python binding of libswiftspec.so: the tree-verification step of
+speculative decoding on AMD Instinct MI355X (gfx950).
+
+Argument marshalling only: every computation runs in the library's HIP
+kernels.  PyTorch supplies device memory and the current HIP stream; the
+functions below pass tensor pointers, shapes and the stream handle through
+the C ABI declared in ``include/swiftspec.h`` and raise ``SwiftSpecError``
+on a non-zero status.  There is no fallback: if the compiled library is
+missing, importing a function raises.
+
+fp16 tensors may be ``torch.float16`` or ``torch.int16``/``torch.uint16``
+views of the same bits.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_build", "libswiftspec.so")
+
+_lib = None
+
+i32, i64, f32, f64, vp, sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
+                              ctypes.c_void_p, ctypes.c_size_t)
+
+OK, INVALID_ARG, UNSUPPORTED, MISALIGNED, WORKSPACE_TOO_SMALL, BAD_TREE, HIP_ERROR = range(7)
+DEVERR_BAD_TREE, DEVERR_BAD_PREFIX, DEVERR_BAD_ACCEPTED = 1, 2, 4
+WS_HEADER_BYTES = 65536
+MAX_TREE = 64
+MAX_M = 64
+
+
+class SwiftSpecError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = _load().swiftspec_status_string(status).decode()
+        if status == HIP_ERROR:
+            msg += f" (hipError {_load().swiftspec_last_hip_error()})"
+        super().__init__(f"{where}: {msg} [status {status}]")
+        self.status = status
+
+
+class W4(ctypes.Structure):
+    _fields_ = [("qweight", vp), ("scales", vp), ("zeros", vp), ("K", i32), ("N", i32)]
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("H", i32), ("Hq", i32), ("Hkv", i32), ("D", i32), ("F", i32), ("S_max", i32),
+                ("eps", f32), ("rope_theta", f32)]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("attn_norm", vp), ("mlp_norm", vp), ("wqkv", W4), ("wo", W4), ("wgate", W4),
+                ("wup", W4), ("wdown", W4), ("k_cache", vp), ("v_cache", vp)]
+
+
+_SIGS = {
+    "swiftspec_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "swiftspec_last_hip_error": ([], ctypes.c_int),
+    "swiftspec_workspace_init": ([vp, sz, vp], ctypes.c_int),
+    "swiftspec_read_device_error": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
+    "swiftspec_w4a16_gemm": ([ctypes.POINTER(W4), vp, i32, i32, vp, i32, vp, i32, vp, sz, vp], ctypes.c_int),
+    "swiftspec_w4a16_gemm_workspace_bytes": ([i32, i32, i32], sz),
+    "swiftspec_w4a16_swiglu": ([ctypes.POINTER(W4), ctypes.POINTER(W4), vp, i32, i32, vp, i32, vp, sz, vp],
+                               ctypes.c_int),
+    "swiftspec_w4a16_swiglu_workspace_bytes": ([i32, i32, i32], sz),
+    "swiftspec_rmsnorm": ([vp, i32, i32, i32, vp, f32, vp, i32, vp], ctypes.c_int),
+    "swiftspec_tree_attention": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, f32,
+                                  vp, i32, vp, sz, vp], ctypes.c_int),
+    "swiftspec_tree_attention_workspace_bytes": ([i32, i32, i32, i32, i32], sz),
+    "swiftspec_rope_table": ([f64, i32, i32, vp], ctypes.c_int),
+    "swiftspec_tree_masks": ([vp, i32, i32, vp, vp, vp, vp], ctypes.c_int),
+    "swiftspec_tree_validate": ([vp, i32, vp], ctypes.c_int),
+    "swiftspec_kv_commit": ([vp, vp, i32, i64, i32, i32, i32, vp, vp, i32, vp, i32, vp, sz, vp], ctypes.c_int),
+    "swiftspec_verify_layer": ([ctypes.POINTER(Layer), ctypes.POINTER(Dims), vp, i32, vp, vp, vp, vp, sz, vp],
+                               ctypes.c_int),
+    "swiftspec_verify_layer_workspace_bytes": ([ctypes.POINTER(Dims), i32], sz),
+    "swiftspec_verify_layer_workspace_layout": ([ctypes.POINTER(Dims), i32, ctypes.POINTER(sz)], ctypes.c_int),
+    "swiftspec_lm_head": ([vp, i32, i32, vp, f32, vp, i32, vp, vp, sz, vp], ctypes.c_int),
+    "swiftspec_lm_head_workspace_bytes": ([i32, i32, i32], sz),
+    "swiftspec_graph_begin": ([vp], ctypes.c_int),
+    "swiftspec_graph_end": ([vp, ctypes.POINTER(vp)], ctypes.c_int),
+    "swiftspec_graph_launch": ([vp, vp], ctypes.c_int),
+    "swiftspec_graph_destroy": ([vp], ctypes.c_int),
+}
+EXPORTS = tuple(_SIGS)
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libswiftspec.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (args, res) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def lib():
+    return _load()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise SwiftSpecError(status, where)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ------------------------------------------------------------------ helpers
+
+def workspace(nbytes: int, device="cuda"):
+    """A zero-filled device workspace (its header counters start at zero)."""
+    import torch
+    return torch.zeros(int(nbytes), dtype=torch.uint8, device=device)
+
+
+def make_w4(qweight, scales, zeros) -> W4:
+    """Describe an int4 matrix held in device tensors qweight [N][K/2] u8,
+    scales [N][K/128] fp16, zeros [N][K/128] u8."""
+    N, half_k = qweight.shape
+    return W4(qweight.data_ptr(), scales.data_ptr(), zeros.data_ptr(), 2 * half_k, N)
+
+
+def rope_table(theta: float, S_max: int, D: int):
+    """Host fp32 (cos, sin) table [S_max][D/2][2] built in fp64 by the library."""
+    import numpy as np
+    out = np.empty((S_max, D // 2, 2), np.float32)
+    _check(_load().swiftspec_rope_table(theta, S_max, D, out.ctypes.data), "rope_table")
+    return out
+
+
+def tree_validate(parent):
+    import numpy as np
+    p = np.ascontiguousarray(parent, dtype=np.int32)
+    depth = np.empty(len(p), np.int32)
+    st = _load().swiftspec_tree_validate(p.ctypes.data, len(p), depth.ctypes.data)
+    return st, depth
+
+
+def read_device_error(ws, stream=None) -> int:
+    out = ctypes.c_uint32(0)
+    _check(_load().swiftspec_read_device_error(_ptr(ws), _stream(stream), ctypes.byref(out)),
+           "read_device_error")
+    return int(out.value)
+
+
+def workspace_init(ws, stream=None):
+    _check(_load().swiftspec_workspace_init(_ptr(ws), ws.numel(), _stream(stream)), "workspace_init")
+
+
+# ------------------------------------------------------------ operations
+
+def gemm_workspace_bytes(M: int, K: int, N: int) -> int:
+    return int(_load().swiftspec_w4a16_gemm_workspace_bytes(M, K, N))
+
+
+def swiglu_workspace_bytes(M: int, K: int, N: int) -> int:
+    return int(_load().swiftspec_w4a16_swiglu_workspace_bytes(M, K, N))
+
+
+def w4a16_gemm(W: W4, x, y, ws, residual=None, stream=None):
+    M, ldx = x.shape[0], x.stride(0)
+    st = _load().swiftspec_w4a16_gemm(ctypes.byref(W), _ptr(x), M, ldx, _ptr(y), y.stride(0),
+                                      _ptr(residual), residual.stride(0) if residual is not None else 0,
+                                      _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "w4a16_gemm")
+
+
+def w4a16_swiglu(Wg: W4, Wu: W4, x, y, ws, stream=None):
+    st = _load().swiftspec_w4a16_swiglu(ctypes.byref(Wg), ctypes.byref(Wu), _ptr(x), x.shape[0],
+                                        x.stride(0), _ptr(y), y.stride(0), _ptr(ws), ws.numel(),
+                                        _stream(stream))
+    _check(st, "w4a16_swiglu")
+
+
+def rmsnorm(x, gamma, out, eps=1e-5, stream=None):
+    st = _load().swiftspec_rmsnorm(_ptr(x), x.shape[0], x.shape[1], x.stride(0), _ptr(gamma), eps,
+                                   _ptr(out), out.stride(0), _stream(stream))
+    _check(st, "rmsnorm")
+
+
+def tree_attention_workspace_bytes(T, Hq, Hkv, D, S_max) -> int:
+    return int(_load().swiftspec_tree_attention_workspace_bytes(T, Hq, Hkv, D, S_max))
+
+
+def tree_attention(q, k, v, k_cache, v_cache, prefix_len, parent, Hq, Hkv, D, rope, out, ws,
+                   softmax_scale=None, stream=None):
+    """q [T][>=Hq*D], k/v [T][>=Hkv*D] (row strides are the leading dims),
+    caches [Hkv][S_max][D], prefix_len int32[1] and parent int32[T] on device."""
+    T = parent.shape[0]
+    S_max = k_cache.shape[-2]
+    if softmax_scale is None:
+        softmax_scale = 1.0 / (D ** 0.5)
+    st = _load().swiftspec_tree_attention(_ptr(q), q.stride(0), _ptr(k), _ptr(v), k.stride(0),
+                                          _ptr(k_cache), _ptr(v_cache), S_max, _ptr(prefix_len),
+                                          _ptr(parent), T, Hq, Hkv, D, _ptr(rope), softmax_scale,
+                                          _ptr(out), out.stride(0), _ptr(ws), ws.numel(),
+                                          _stream(stream))
+    _check(st, "tree_attention")
+
+
+def tree_masks(parents, anc, depth, status, stream=None):
+    n, T = parents.shape
+    st = _load().swiftspec_tree_masks(_ptr(parents), n, T, _ptr(anc), _ptr(depth), _ptr(status),
+                                      _stream(stream))
+    _check(st, "tree_masks")
+
+
+def kv_commit(k_cache, v_cache, prefix_len, parent, accepted, n_layers=1, layer_stride=None,
+              advance=False, ws=None, stream=None):
+    """Caches [n_layers][Hkv][S_max][D] (or [Hkv][S_max][D]); prefix_len,
+    parent and accepted are device int32 tensors."""
+    Hkv, S_max, D = k_cache.shape[-3:]
+    if layer_stride is None:
+        layer_stride = Hkv * S_max * D
+    st = _load().swiftspec_kv_commit(_ptr(k_cache), _ptr(v_cache), n_layers, layer_stride, Hkv, S_max,
+                                     D, _ptr(prefix_len), _ptr(parent), parent.shape[0], _ptr(accepted),
+                                     int(bool(advance)), _ptr(ws), ws.numel() if ws is not None else 0,
+                                     _stream(stream))
+    _check(st, "kv_commit")
+
+
+def make_dims(H, Hq, Hkv, D, F, S_max, eps=1e-5, rope_theta=500000.0) -> Dims:
+    return Dims(H, Hq, Hkv, D, F, S_max, eps, rope_theta)
+
+
+def make_layer(attn_norm, mlp_norm, wqkv: W4, wo: W4, wgate: W4, wup: W4, wdown: W4, k_cache,
+               v_cache) -> Layer:
+    return Layer(attn_norm.data_ptr(), mlp_norm.data_ptr(), wqkv, wo, wgate, wup, wdown,
+                 k_cache.data_ptr(), v_cache.data_ptr())
+
+
+def verify_layer_workspace_bytes(dims: Dims, T: int) -> int:
+    return int(_load().swiftspec_verify_layer_workspace_bytes(ctypes.byref(dims), T))
+
+
+def verify_layer_intermediates(dims: Dims, T: int, ws):
+    """Views (int16 bits) of the layer intermediates xn, qkv, o, h, hn, m
+    held in a verify_layer workspace."""
+    offs = (sz * 6)()
+    _check(_load().swiftspec_verify_layer_workspace_layout(ctypes.byref(dims), T, offs),
+           "verify_layer_workspace_layout")
+    import torch
+    n_qkv = (dims.Hq + 2 * dims.Hkv) * dims.D
+    cols = [dims.H, n_qkv, dims.Hq * dims.D, dims.H, dims.H, dims.F]
+    names = ["xn", "qkv", "o", "h", "hn", "m"]
+    out = {}
+    for name, off, c in zip(names, offs, cols):
+        out[name] = ws[off:off + T * c * 2].view(torch.int16).view(T, c)
+    return out
+
+
+def verify_layer(layer: Layer, dims: Dims, hidden, prefix_len, parent, rope, ws, stream=None):
+    st = _load().swiftspec_verify_layer(ctypes.byref(layer), ctypes.byref(dims), _ptr(hidden),
+                                        hidden.shape[0], _ptr(prefix_len), _ptr(parent), _ptr(rope),
+                                        _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "verify_layer")
+
+
+def lm_head_workspace_bytes(M, H, V) -> int:
+    return int(_load().swiftspec_lm_head_workspace_bytes(M, H, V))
+
+
+def lm_head(h, gamma, W, logits, ws, eps=1e-5, stream=None):
+    M, H = h.shape
+    V = W.shape[0]
+    st = _load().swiftspec_lm_head(_ptr(h), M, H, _ptr(gamma), eps, _ptr(W), V, _ptr(logits), _ptr(ws),
+                                   ws.numel(), _stream(stream))
+    _check(st, "lm_head")
+
+
+class Graph:
+    """A HIP graph captured from the library calls issued on `stream`
+    between begin() and end()."""
+
+    def __init__(self):
+        self._g = ctypes.c_void_p(None)
+
+    def begin(self, stream=None):
+        _check(_load().swiftspec_graph_begin(_stream(stream)), "graph_begin")
+
+    def end(self, stream=None):
+        _check(_load().swiftspec_graph_end(_stream(stream), ctypes.byref(self._g)), "graph_end")
+
+    def launch(self, stream=None):
+        _check(_load().swiftspec_graph_launch(self._g, _stream(stream)), "graph_launch")
+
+    def __del__(self):
+        if self._g and self._g.value and _lib is not None:
+            _lib.swiftspec_graph_destroy(self._g)
+            self._g = ctypes.c_void_p(None)

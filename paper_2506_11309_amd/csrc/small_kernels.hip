@@ -1,0 +1,173 @@
+// RMSNorm, KV commit, tree-mask query and workspace-initialisation kernels.
+#include "ss_device.h"
+#include "ss_internal.h"
+
+namespace ss {
+
+// ------------------------------------------------------------------ RMSNorm
+// out = fp16(x / sqrt(mean(x^2) + eps) * gamma); one workgroup per row,
+// fp32 sum of squares, fixed reduction order (deterministic).
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x, int H, int ldx,
+                                                      const uint16_t* __restrict__ gamma, float eps,
+                                                      uint16_t* __restrict__ out, int ldo) {
+  __shared__ float partial[4];
+  const int m = blockIdx.x;
+  const uint16_t* xr = x + (size_t)m * ldx;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
+    half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + c));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float v = (float)h[e];
+      ss = __builtin_fmaf(v, v, ss);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
+  if (lane_id() == 0) partial[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float total = (partial[0] + partial[1]) + (partial[2] + partial[3]);
+  const float inv = 1.0f / sqrtf(total / (float)H + eps);
+  uint16_t* orow = out + (size_t)m * ldo;
+  for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
+    half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + c));
+    half8 gm = bitcast<half8>(*reinterpret_cast<const u32x4*>(gamma + c));
+    half8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (_Float16)(((float)h[e] * inv) * (float)gm[e]);
+    *reinterpret_cast<u32x4*>(orow + c) = bitcast<u32x4>(o);
+  }
+}
+
+void launch_rmsnorm(const uint16_t* x, int M, int H, int ldx, const uint16_t* gamma, float eps,
+                    uint16_t* out, int ldo, hipStream_t st) {
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo);
+}
+
+// ---------------------------------------------------------------- KV commit
+// One workgroup per (layer, K|V, kv head).  Wave 0 derives the accepted
+// path from the device parent array: the ancestor-or-self mask of the
+// accepted node, whose set bits in increasing order are the root-to-node
+// path (indices grow along any root path since parent[i] < i).  Every
+// thread then loads its 16-byte column slice of all L source rows into
+// registers; after a barrier it stores them to rows P .. P+L-1, so no write
+// can clobber a source another thread has yet to read.
+constexpr int kCommitMaxRowsPerThread = 8;  // 64 rows, D = 128: 16 B x 8 rows per thread
+
+__device__ __forceinline__ bool commit_setup(const int32_t* parent, int T, const int32_t* accepted,
+                                             const int32_t* prefix_len, int S_max, int* s_path,
+                                             int* s_L, int* s_P, int* s_err) {
+  // wave 0 only
+  uint64_t anc;
+  int depth;
+  const bool ok = tree_masks_wave(parent, T, anc, depth);
+  const int lane = lane_id();
+  const int acc = *accepted;
+  const int P = *prefix_len;
+  int err = 0;
+  if (!ok) err |= SWIFTSPEC_DEVERR_BAD_TREE;
+  if (acc < 0 || acc >= T) err |= SWIFTSPEC_DEVERR_BAD_ACCEPTED;
+  if (P < 0 || P > S_max - T) err |= SWIFTSPEC_DEVERR_BAD_PREFIX;
+  const uint64_t path = shfl_u64(anc, (acc >= 0 && acc < T) ? acc : 0);
+  if (lane < T && ((path >> lane) & 1ull)) {
+    const int rank = __popcll(path & ((1ull << lane) - 1ull));
+    s_path[rank] = lane;
+  }
+  if (lane == 0) {
+    *s_L = __popcll(path);
+    *s_P = P;
+    *s_err = err;
+  }
+  return err == 0;
+}
+
+__global__ __launch_bounds__(256) void kv_commit_kernel(uint16_t* k_cache, uint16_t* v_cache,
+                                                        int64_t layer_stride, int Hkv, int S_max,
+                                                        int D, const int32_t* prefix_len,
+                                                        const int32_t* parent, int T,
+                                                        const int32_t* accepted, void* ws) {
+  __shared__ int s_path[64];
+  __shared__ int s_L, s_P, s_err;
+  const int idx = blockIdx.x;
+  const int head = idx % Hkv;
+  const int which = (idx / Hkv) & 1;
+  const int layer = idx / (2 * Hkv);
+  if (threadIdx.x < 64) commit_setup(parent, T, accepted, prefix_len, S_max, s_path, &s_L, &s_P, &s_err);
+  __syncthreads();
+  if (s_err) {
+    if (idx == 0 && threadIdx.x == 0) report_error(ws, (uint32_t)s_err);
+    return;
+  }
+  const int L = s_L, P = s_P;
+  uint16_t* base = (which ? v_cache : k_cache) + (size_t)layer * layer_stride + ((size_t)head * S_max + P) * D;
+  const int vec_per_row = D / 8;
+  const int rows_per_pass = 256 / vec_per_row;
+  const int c8 = (threadIdx.x % vec_per_row) * 8;
+  const int r0 = threadIdx.x / vec_per_row;
+  u32x4 buf[kCommitMaxRowsPerThread];
+#pragma unroll
+  for (int j = 0; j < kCommitMaxRowsPerThread; ++j) {
+    const int i = r0 + j * rows_per_pass;
+    if (i < L) buf[j] = *reinterpret_cast<const u32x4*>(base + (size_t)s_path[i] * D + c8);
+  }
+  __syncthreads();  // every source row read before any row is written
+#pragma unroll
+  for (int j = 0; j < kCommitMaxRowsPerThread; ++j) {
+    const int i = r0 + j * rows_per_pass;
+    if (i < L) *reinterpret_cast<u32x4*>(base + (size_t)i * D + c8) = buf[j];
+  }
+}
+
+// Advances the device prefix length by the accepted path length (runs after
+// the copy kernel in stream order).
+__global__ void prefix_advance_kernel(int32_t* prefix_len, const int32_t* parent, int T,
+                                      const int32_t* accepted, int S_max) {
+  __shared__ int s_path[64];
+  __shared__ int s_L, s_P, s_err;
+  commit_setup(parent, T, accepted, prefix_len, S_max, s_path, &s_L, &s_P, &s_err);
+  __syncthreads();
+  if (threadIdx.x == 0 && s_err == 0) *prefix_len = s_P + s_L;
+}
+
+void launch_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_t layer_stride,
+                      int Hkv, int S_max, int D, int32_t* prefix_len, const int32_t* parent, int T,
+                      const int32_t* accepted, int advance, void* ws, hipStream_t st) {
+  hipLaunchKernelGGL(kv_commit_kernel, dim3(n_layers * 2 * Hkv), dim3(256), 0, st, k_cache, v_cache,
+                     layer_stride, Hkv, S_max, D, prefix_len, parent, T, accepted, ws);
+  if (advance)
+    hipLaunchKernelGGL(prefix_advance_kernel, dim3(1), dim3(64), 0, st, prefix_len, parent, T, accepted,
+                       S_max);
+}
+
+// ---------------------------------------------------------- tree masks
+__global__ __launch_bounds__(64) void tree_masks_kernel(const int32_t* parents, int T, uint64_t* anc,
+                                                        int32_t* depth, int32_t* status) {
+  const int t = blockIdx.x;
+  uint64_t a;
+  int d;
+  const bool ok = tree_masks_wave(parents + (size_t)t * T, T, a, d);
+  const int lane = lane_id();
+  if (lane < T) {
+    anc[(size_t)t * T + lane] = a;
+    depth[(size_t)t * T + lane] = d;
+  }
+  if (lane == 0) status[t] = ok ? 0 : (int32_t)SWIFTSPEC_DEVERR_BAD_TREE;
+}
+
+void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc, int32_t* depth,
+                       int32_t* status, hipStream_t st) {
+  hipLaunchKernelGGL(tree_masks_kernel, dim3(n_trees), dim3(64), 0, st, parents, T, anc, depth, status);
+}
+
+// ------------------------------------------------------ workspace init
+__global__ void fill_zero_kernel(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+void launch_ws_init(void* ws, size_t bytes, hipStream_t st) {
+  const size_t n = bytes / 4;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, st, reinterpret_cast<uint32_t*>(ws), n);
+}
+
+}  // namespace ss

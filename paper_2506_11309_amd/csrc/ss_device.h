@@ -1,0 +1,129 @@
+// Device-side helpers shared by the swiftspec HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/swiftspec.h"
+
+namespace ss {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// Workspace header: error word at byte 0, ticket counters from byte 256.
+constexpr uint32_t kWsHeaderBytes = 65536u;
+constexpr uint32_t kWsCounterOffset = 256u;
+constexpr uint32_t kWsMaxCounters = (kWsHeaderBytes - kWsCounterOffset) / 4u;
+
+__device__ __forceinline__ uint32_t* ws_error_word(void* ws) { return reinterpret_cast<uint32_t*>(ws); }
+__device__ __forceinline__ uint32_t* ws_counters(void* ws) {
+  return reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + kWsCounterOffset);
+}
+
+__device__ __forceinline__ void report_error(void* ws, uint32_t bits) {
+  if (ws) __hip_atomic_fetch_or(ws_error_word(ws), bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  uint32_t lo = __shfl((int)(uint32_t)v, src, kWave);
+  uint32_t hi = __shfl((int)(uint32_t)(v >> 32), src, kWave);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Ancestor-or-self bitmask and depth of node `lane` (lane < T <= 64) for the
+// parent array `parent` (global memory), computed by one full wavefront with
+// pointer jumping: after round r every lane holds the 2^r nearest nodes of
+// its root path, so 6 rounds cover any depth below 64.  Must be called by
+// all 64 lanes of a wave.  Returns false (for every lane) if the array is
+// not a valid increasing tree; then anc = own bit and depth = 0.
+__device__ __forceinline__ bool tree_masks_wave(const int32_t* __restrict__ parent, int T,
+                                                uint64_t& anc, int& depth) {
+  const int lane = lane_id();
+  int p = -1;
+  if (lane < T) p = parent[lane];
+  bool ok = lane >= T || (lane == 0 ? p == -1 : (p >= 0 && p < lane));
+  const bool all_ok = __all(ok);
+  uint64_t a = lane < T ? (1ull << lane) : 0ull;
+  if (!all_ok) {
+    anc = a;
+    depth = 0;
+    return false;
+  }
+  int up = lane < T ? p : -1;
+#pragma unroll
+  for (int r = 0; r < 6; ++r) {
+    const int src = up >= 0 ? up : lane;
+    const uint64_t a_up = shfl_u64(a, src);
+    const int up_up = __shfl(up, src, kWave);
+    if (up >= 0) {
+      a |= a_up;
+      up = up_up;
+    }
+  }
+  anc = a;
+  depth = __popcll(a) - 1;
+  return true;
+}
+
+// fp16 bit helpers
+__device__ __forceinline__ float h2f(uint16_t h) {
+  _Float16 v;
+  __builtin_memcpy(&v, &h, 2);
+  return (float)v;
+}
+__device__ __forceinline__ uint16_t f2h(float f) {
+  _Float16 v = (_Float16)f;  // round to nearest even
+  uint16_t h;
+  __builtin_memcpy(&h, &v, 2);
+  return h;
+}
+
+template <typename V, typename S>
+__device__ __forceinline__ V bitcast(const S& s) {
+  static_assert(sizeof(V) == sizeof(S), "size mismatch");
+  V v;
+  __builtin_memcpy(&v, &s, sizeof(V));
+  return v;
+}
+
+// Agent-scope (cross-XCD) coherent 8-byte store / load for split partials.
+__device__ __forceinline__ void store_agent_u64(void* p, uint64_t v) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t load_agent_u64(const void* p) {
+  return __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_agent_f32x4(float* p, f32x4 v) {
+  store_agent_u64(p, bitcast<uint64_t>(f32x2{v[0], v[1]}));
+  store_agent_u64(p + 2, bitcast<uint64_t>(f32x2{v[2], v[3]}));
+}
+__device__ __forceinline__ f32x4 load_agent_f32x4(const float* p) {
+  f32x2 a = bitcast<f32x2>(load_agent_u64(p));
+  f32x2 b = bitcast<f32x2>(load_agent_u64(p + 2));
+  return f32x4{a[0], a[1], b[0], b[1]};
+}
+
+// Wait until every outstanding memory operation of this wave has completed
+// (stores acknowledged at their coherence scope).
+__device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Ticket for the deterministic "last arriving workgroup combines" pattern.
+// Called by one lane after the workgroup's partial stores completed.
+__device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
+  return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void reset_counter(uint32_t* counter) {
+  __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+}  // namespace ss

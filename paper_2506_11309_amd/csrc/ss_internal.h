@@ -1,0 +1,95 @@
+// Host-side launch descriptors shared between the C-ABI layer and the
+// kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ss {
+
+struct W4Host {
+  const uint8_t* q;
+  const uint16_t* s;
+  const uint8_t* z;
+};
+
+struct GemmLaunch {
+  W4Host w0, w1;  // w1: up-projection of the fused SwiGLU
+  int K, N;       // N = output columns
+  const uint16_t* x;
+  int M, ldx;
+  uint16_t* y;
+  int ldy;
+  const uint16_t* res;
+  int ldr;
+  int nw;       // N-tiles (16 columns) per workgroup, counting gate and up tiles for SwiGLU
+  int nblocks;  // column blocks
+  int nsplit;   // K-splits
+  bool swiglu;
+  float* part;
+  uint32_t* counters;
+};
+
+struct GemmPlan {
+  int nw, nblocks, nsplit;
+  size_t part_bytes;
+};
+GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu);
+void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st);
+
+struct DenseGemmLaunch {
+  const uint16_t* w;  // [N][K] fp16
+  int K, N;
+  const uint16_t* x;
+  int M, ldx;
+  uint16_t* y;
+  int ldy;
+  int nw, nblocks, nsplit;
+  float* part;
+  uint32_t* counters;
+};
+GemmPlan plan_dense_gemm(int M, int K, int N);
+void launch_dense_gemm(const DenseGemmLaunch& L, hipStream_t st);
+
+struct AttnLaunch {
+  const uint16_t* q;
+  int ldq;
+  const uint16_t* k;
+  const uint16_t* v;
+  int ldkv;
+  uint16_t* k_cache;
+  uint16_t* v_cache;
+  int S_max;
+  const int32_t* prefix_len;
+  const int32_t* parent;
+  int T, Hq, Hkv, D;
+  const float* rope;
+  float scale;
+  uint16_t* out;
+  int ldo;
+  void* ws;         // header (error word, counters)
+  float* part;      // split partials
+  int nsplit;       // key splits per kv head
+  int chunk;        // prefix keys per split (multiple of the key tile)
+};
+struct AttnPlan {
+  int nsplit, chunk;
+  size_t part_bytes;
+};
+AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max);
+void launch_tree_attention(const AttnLaunch& L, hipStream_t st);
+
+void launch_rmsnorm(const uint16_t* x, int M, int H, int ldx, const uint16_t* gamma, float eps,
+                    uint16_t* out, int ldo, hipStream_t st);
+
+void launch_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_t layer_stride,
+                      int Hkv, int S_max, int D, int32_t* prefix_len, const int32_t* parent, int T,
+                      const int32_t* accepted, int advance, void* ws, hipStream_t st);
+
+void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc, int32_t* depth,
+                       int32_t* status, hipStream_t st);
+
+void launch_ws_init(void* ws, size_t bytes, hipStream_t st);
+
+}  // namespace ss

@@ -1,0 +1,468 @@
+// C-ABI layer of libswiftspec.so: argument validation, workspace planning,
+// kernel launches on the caller's stream, and HIP-graph helpers.
+// The contract of every entry point is documented in include/swiftspec.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "../../include/swiftspec.h"
+#include "ss_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr size_t kHeader = SWIFTSPEC_WS_HEADER_BYTES;
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+int check_launch() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    g_last_hip_error = (int)e;
+    return SWIFTSPEC_HIP_ERROR;
+  }
+  return SWIFTSPEC_OK;
+}
+
+int hip_status(hipError_t e) {
+  if (e != hipSuccess) {
+    g_last_hip_error = (int)e;
+    return SWIFTSPEC_HIP_ERROR;
+  }
+  return SWIFTSPEC_OK;
+}
+
+int check_w4(const swiftspec_w4* W) {
+  if (!W || !W->qweight || !W->scales || !W->zeros) return SWIFTSPEC_INVALID_ARG;
+  if (W->K <= 0 || W->N <= 0) return SWIFTSPEC_INVALID_ARG;
+  if (W->K % 128 != 0 || W->N % 16 != 0) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(W->qweight)) return SWIFTSPEC_MISALIGNED;
+  return SWIFTSPEC_OK;
+}
+
+constexpr int kMaxCounters = (int)((SWIFTSPEC_WS_HEADER_BYTES - 256u) / 4u);
+
+bool gemm_counters_fit(int M, int K, int N, bool swiglu) {
+  return ss::plan_w4a16_gemm(M, K, N, swiglu).nblocks <= kMaxCounters;
+}
+
+bool attn_counters_fit(int T, int Hq, int Hkv) {
+  const long R = (long)T * (Hq / Hkv);
+  return (long)Hkv * ((R + 63) / 64) <= kMaxCounters;
+}
+
+size_t gemm_ws(int M, int K, int N, bool swiglu) {
+  ss::GemmPlan p = ss::plan_w4a16_gemm(M, K, N, swiglu);
+  return kHeader + align_up(p.part_bytes);
+}
+
+// Launch a validated W4A16 GEMM / SwiGLU with partials in `part`.
+void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* x, int M, int ldx,
+              uint16_t* y, int ldy, const uint16_t* res, int ldr, void* ws, float* part,
+              hipStream_t st) {
+  const bool swiglu = W1 != nullptr;
+  ss::GemmPlan p = ss::plan_w4a16_gemm(M, W0->K, W0->N, swiglu);
+  ss::GemmLaunch L;
+  L.w0 = {W0->qweight, W0->scales, W0->zeros};
+  L.w1 = swiglu ? ss::W4Host{W1->qweight, W1->scales, W1->zeros} : L.w0;
+  L.K = W0->K;
+  L.N = W0->N;
+  L.x = x;
+  L.M = M;
+  L.ldx = ldx;
+  L.y = y;
+  L.ldy = ldy;
+  L.res = res;
+  L.ldr = ldr;
+  L.nw = p.nw;
+  L.nblocks = p.nblocks;
+  L.nsplit = p.nsplit;
+  L.swiglu = swiglu;
+  L.part = part;
+  L.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + 256);
+  ss::launch_w4a16_gemm(L, st);
+}
+
+int check_tree_attention_args(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v,
+                              int ldkv, const uint16_t* kc, const uint16_t* vc, int S_max,
+                              const int32_t* P, const int32_t* parent, int T, int Hq, int Hkv,
+                              int D, const float* rope, const uint16_t* out, int ldo) {
+  if (!q || !k || !v || !kc || !vc || !P || !parent || !rope || !out) return SWIFTSPEC_INVALID_ARG;
+  if (T < 1 || Hq < 1 || Hkv < 1 || S_max < T) return SWIFTSPEC_INVALID_ARG;
+  if (T > SWIFTSPEC_MAX_TREE || (D != 64 && D != 128) || Hq % Hkv != 0) return SWIFTSPEC_UNSUPPORTED;
+  if (ldq < Hq * D || ldkv < Hkv * D || ldo < Hq * D) return SWIFTSPEC_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(kc) || !aligned16(vc))
+    return SWIFTSPEC_MISALIGNED;
+  if (ldq % 8 || ldkv % 8) return SWIFTSPEC_MISALIGNED;
+  if (!attn_counters_fit(T, Hq, Hkv)) return SWIFTSPEC_UNSUPPORTED;
+  return SWIFTSPEC_OK;
+}
+
+size_t attn_ws(int T, int Hq, int Hkv, int D, int S_max) {
+  ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max);
+  return kHeader + align_up(p.part_bytes);
+}
+
+void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v, int ldkv,
+                   uint16_t* kc, uint16_t* vc, int S_max, const int32_t* P, const int32_t* parent,
+                   int T, int Hq, int Hkv, int D, const float* rope, float scale, uint16_t* out,
+                   int ldo, void* ws, float* part, hipStream_t st) {
+  ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max);
+  ss::AttnLaunch L;
+  L.q = q;
+  L.ldq = ldq;
+  L.k = k;
+  L.v = v;
+  L.ldkv = ldkv;
+  L.k_cache = kc;
+  L.v_cache = vc;
+  L.S_max = S_max;
+  L.prefix_len = P;
+  L.parent = parent;
+  L.T = T;
+  L.Hq = Hq;
+  L.Hkv = Hkv;
+  L.D = D;
+  L.rope = rope;
+  L.scale = scale;
+  L.out = out;
+  L.ldo = ldo;
+  L.ws = ws;
+  L.part = part;
+  L.nsplit = p.nsplit;
+  L.chunk = p.chunk;
+  ss::launch_tree_attention(L, st);
+}
+
+struct LayerWs {
+  size_t xn, qkv, o, h, hn, m, part, total;
+};
+
+LayerWs layer_ws(const swiftspec_dims* d, int T) {
+  LayerWs w;
+  const int Nqkv = (d->Hq + 2 * d->Hkv) * d->D;
+  size_t off = kHeader;
+  w.xn = off;
+  off += align_up((size_t)T * d->H * 2);
+  w.qkv = off;
+  off += align_up((size_t)T * Nqkv * 2);
+  w.o = off;
+  off += align_up((size_t)T * d->Hq * d->D * 2);
+  w.h = off;
+  off += align_up((size_t)T * d->H * 2);
+  w.hn = off;
+  off += align_up((size_t)T * d->H * 2);
+  w.m = off;
+  off += align_up((size_t)T * d->F * 2);
+  size_t part = 0;
+  auto upd = [&](size_t b) { part = b > part ? b : part; };
+  upd(ss::plan_w4a16_gemm(T, d->H, Nqkv, false).part_bytes);
+  upd(ss::plan_w4a16_gemm(T, d->Hq * d->D, d->H, false).part_bytes);
+  upd(ss::plan_w4a16_gemm(T, d->H, d->F, true).part_bytes);
+  upd(ss::plan_w4a16_gemm(T, d->F, d->H, false).part_bytes);
+  upd(ss::plan_tree_attention(T, d->Hq, d->Hkv, d->D, d->S_max).part_bytes);
+  w.part = off;
+  off += align_up(part);
+  w.total = off;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* swiftspec_status_string(int status) {
+  switch (status) {
+    case SWIFTSPEC_OK: return "ok";
+    case SWIFTSPEC_INVALID_ARG: return "invalid argument";
+    case SWIFTSPEC_UNSUPPORTED: return "unsupported shape";
+    case SWIFTSPEC_MISALIGNED: return "misaligned pointer or leading dimension";
+    case SWIFTSPEC_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case SWIFTSPEC_BAD_TREE: return "invalid parent array";
+    case SWIFTSPEC_HIP_ERROR: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int swiftspec_last_hip_error(void) { return g_last_hip_error; }
+
+int swiftspec_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+  if (!ws || ws_bytes < kHeader) return SWIFTSPEC_INVALID_ARG;
+  ss::launch_ws_init(ws, kHeader, S(stream));
+  return check_launch();
+}
+
+int swiftspec_read_device_error(void* ws, void* stream, uint32_t* out) {
+  if (!ws || !out) return SWIFTSPEC_INVALID_ARG;
+  int rc = hip_status(hipStreamSynchronize(S(stream)));
+  if (rc) return rc;
+  rc = hip_status(hipMemcpy(out, ws, sizeof(uint32_t), hipMemcpyDeviceToHost));
+  if (rc) return rc;
+  ss::launch_ws_init(ws, 256, S(stream));
+  rc = check_launch();
+  if (rc) return rc;
+  return hip_status(hipStreamSynchronize(S(stream)));
+}
+
+size_t swiftspec_w4a16_gemm_workspace_bytes(int32_t M, int32_t K, int32_t N) {
+  if (M < 1 || K < 128 || N < 16) return kHeader;
+  return gemm_ws(M, K, N, false);
+}
+
+size_t swiftspec_w4a16_swiglu_workspace_bytes(int32_t M, int32_t K, int32_t N) {
+  if (M < 1 || K < 128 || N < 16) return kHeader;
+  return gemm_ws(M, K, N, true);
+}
+
+int swiftspec_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, int32_t ldx,
+                         uint16_t* y, int32_t ldy, const uint16_t* residual, int32_t ldr,
+                         void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_w4(W);
+  if (rc) return rc;
+  if (!x || !y || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (M < 0 || ldx < W->K || ldy < W->N || (residual && ldr < W->N)) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(x) || ldx % 8) return SWIFTSPEC_MISALIGNED;
+  if (residual == y && ldr != ldy) return SWIFTSPEC_INVALID_ARG;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (!gemm_counters_fit(M, W->K, W->N, false)) return SWIFTSPEC_UNSUPPORTED;
+  if (ws_bytes < gemm_ws(M, W->K, W->N, false)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  run_gemm(W, nullptr, x, M, ldx, y, ldy, residual, ldr, ws,
+           reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
+  return check_launch();
+}
+
+int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* x,
+                           int32_t M, int32_t ldx, uint16_t* y, int32_t ldy, void* ws,
+                           size_t ws_bytes, void* stream) {
+  int rc = check_w4(Wg);
+  if (rc) return rc;
+  rc = check_w4(Wu);
+  if (rc) return rc;
+  if (Wg->K != Wu->K || Wg->N != Wu->N) return SWIFTSPEC_INVALID_ARG;
+  if (!x || !y || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (M < 0 || ldx < Wg->K || ldy < Wg->N) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(x) || ldx % 8) return SWIFTSPEC_MISALIGNED;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (!gemm_counters_fit(M, Wg->K, Wg->N, true)) return SWIFTSPEC_UNSUPPORTED;
+  if (ws_bytes < gemm_ws(M, Wg->K, Wg->N, true)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  run_gemm(Wg, Wu, x, M, ldx, y, ldy, nullptr, 0, ws,
+           reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
+  return check_launch();
+}
+
+int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, const uint16_t* gamma,
+                      float eps, uint16_t* out, int32_t ldo, void* stream) {
+  if (!x || !gamma || !out || M < 0 || H <= 0 || ldx < H || ldo < H) return SWIFTSPEC_INVALID_ARG;
+  if (H % 8) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(gamma) || !aligned16(out) || ldx % 8 || ldo % 8)
+    return SWIFTSPEC_MISALIGNED;
+  if (M == 0) return SWIFTSPEC_OK;
+  ss::launch_rmsnorm(x, M, H, ldx, gamma, eps, out, ldo, S(stream));
+  return check_launch();
+}
+
+size_t swiftspec_tree_attention_workspace_bytes(int32_t T, int32_t Hq, int32_t Hkv, int32_t D,
+                                                int32_t S_max) {
+  if (T < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (D != 64 && D != 128) || S_max < T) return kHeader;
+  return attn_ws(T, Hq, Hkv, D, S_max);
+}
+
+int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                             int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
+                             const int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,
+                             int32_t Hq, int32_t Hkv, int32_t D, const float* rope_cos_sin,
+                             float softmax_scale, uint16_t* out, int32_t ldo, void* ws,
+                             size_t ws_bytes, void* stream) {
+  int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len,
+                                     d_parent, T, Hq, Hkv, D, rope_cos_sin, out, ldo);
+  if (rc) return rc;
+  if (!ws) return SWIFTSPEC_INVALID_ARG;
+  if (ws_bytes < attn_ws(T, Hq, Hkv, D, S_max)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  run_attention(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_parent, T, Hq, Hkv, D,
+                rope_cos_sin, softmax_scale, out, ldo, ws,
+                reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
+  return check_launch();
+}
+
+int swiftspec_rope_table(double theta, int32_t S_max, int32_t D, float* host_out) {
+  if (!host_out || S_max < 1 || D < 2 || D % 2 || !(theta > 0)) return SWIFTSPEC_INVALID_ARG;
+  const int half = D / 2;
+  for (int d = 0; d < half; ++d) {
+    const double inv_freq = std::pow(theta, -2.0 * d / (double)D);
+    for (int pos = 0; pos < S_max; ++pos) {
+      const double ang = (double)pos * inv_freq;
+      host_out[((size_t)pos * half + d) * 2 + 0] = (float)std::cos(ang);
+      host_out[((size_t)pos * half + d) * 2 + 1] = (float)std::sin(ang);
+    }
+  }
+  return SWIFTSPEC_OK;
+}
+
+int swiftspec_tree_masks(const int32_t* d_parents, int32_t n_trees, int32_t T, uint64_t* d_anc,
+                         int32_t* d_depth, int32_t* d_status, void* stream) {
+  if (!d_parents || !d_anc || !d_depth || !d_status || n_trees < 0 || T < 1) return SWIFTSPEC_INVALID_ARG;
+  if (T > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_UNSUPPORTED;
+  if (n_trees == 0) return SWIFTSPEC_OK;
+  ss::launch_tree_masks(d_parents, n_trees, T, d_anc, d_depth, d_status, S(stream));
+  return check_launch();
+}
+
+int swiftspec_tree_validate(const int32_t* parent, int32_t T, int32_t* depth_out) {
+  if (!parent || T < 1) return SWIFTSPEC_INVALID_ARG;
+  if (parent[0] != -1) return SWIFTSPEC_BAD_TREE;
+  for (int i = 1; i < T; ++i)
+    if (parent[i] < 0 || parent[i] >= i) return SWIFTSPEC_BAD_TREE;
+  if (depth_out) {
+    depth_out[0] = 0;
+    for (int i = 1; i < T; ++i) depth_out[i] = depth_out[parent[i]] + 1;
+  }
+  return SWIFTSPEC_OK;
+}
+
+int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
+                        int64_t layer_stride_elems, int32_t Hkv, int32_t S_max, int32_t D,
+                        int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,
+                        const int32_t* d_accepted_node, int32_t advance, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (!k_cache || !v_cache || !d_prefix_len || !d_parent || !d_accepted_node) return SWIFTSPEC_INVALID_ARG;
+  if (n_layers < 1 || Hkv < 1 || T < 1 || S_max < T || D < 8) return SWIFTSPEC_INVALID_ARG;
+  if (layer_stride_elems < (int64_t)Hkv * S_max * D) return SWIFTSPEC_INVALID_ARG;
+  if (T > SWIFTSPEC_MAX_TREE || D % 8 || D > 256) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || layer_stride_elems % 8) return SWIFTSPEC_MISALIGNED;
+  if (ws && ws_bytes < kHeader) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  if ((int64_t)n_layers * 2 * Hkv > 0x7fffffff) return SWIFTSPEC_UNSUPPORTED;
+  ss::launch_kv_commit(k_cache, v_cache, n_layers, layer_stride_elems, Hkv, S_max, D, d_prefix_len,
+                       d_parent, T, d_accepted_node, advance, ws, S(stream));
+  return check_launch();
+}
+
+size_t swiftspec_verify_layer_workspace_bytes(const swiftspec_dims* dims, int32_t T) {
+  if (!dims || T < 1 || T > SWIFTSPEC_MAX_TREE) return kHeader;
+  return layer_ws(dims, T).total;
+}
+
+int swiftspec_verify_layer_workspace_layout(const swiftspec_dims* dims, int32_t T, size_t* offsets) {
+  if (!dims || !offsets || T < 1 || T > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_INVALID_ARG;
+  const LayerWs w = layer_ws(dims, T);
+  offsets[0] = w.xn;
+  offsets[1] = w.qkv;
+  offsets[2] = w.o;
+  offsets[3] = w.h;
+  offsets[4] = w.hn;
+  offsets[5] = w.m;
+  return SWIFTSPEC_OK;
+}
+
+int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, uint16_t* hidden,
+                           int32_t T, const int32_t* d_prefix_len, const int32_t* d_parent,
+                           const float* rope, void* ws, size_t ws_bytes, void* stream) {
+  if (!Lw || !d || !hidden || !d_prefix_len || !d_parent || !rope || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (!Lw->attn_norm || !Lw->mlp_norm || !Lw->k_cache || !Lw->v_cache) return SWIFTSPEC_INVALID_ARG;
+  if (T < 1 || d->H < 1 || d->Hq < 1 || d->Hkv < 1 || d->F < 1 || d->S_max < T) return SWIFTSPEC_INVALID_ARG;
+  if (T > SWIFTSPEC_MAX_TREE || (d->D != 64 && d->D != 128) || d->Hq % d->Hkv) return SWIFTSPEC_UNSUPPORTED;
+  const int H = d->H, Hd = d->Hq * d->D, Nqkv = (d->Hq + 2 * d->Hkv) * d->D, F = d->F;
+  if (!attn_counters_fit(T, d->Hq, d->Hkv) || !gemm_counters_fit(T, F, H, false) ||
+      !gemm_counters_fit(T, H, F, true) || !gemm_counters_fit(T, H, Nqkv, false))
+    return SWIFTSPEC_UNSUPPORTED;
+  int rc;
+  if ((rc = check_w4(&Lw->wqkv)) || (rc = check_w4(&Lw->wo)) || (rc = check_w4(&Lw->wgate)) ||
+      (rc = check_w4(&Lw->wup)) || (rc = check_w4(&Lw->wdown)))
+    return rc;
+  if (Lw->wqkv.K != H || Lw->wqkv.N != Nqkv || Lw->wo.K != Hd || Lw->wo.N != H ||
+      Lw->wgate.K != H || Lw->wgate.N != F || Lw->wup.K != H || Lw->wup.N != F ||
+      Lw->wdown.K != F || Lw->wdown.N != H)
+    return SWIFTSPEC_INVALID_ARG;
+  if (!aligned16(hidden) || !aligned16(Lw->attn_norm) || !aligned16(Lw->mlp_norm) ||
+      !aligned16(Lw->k_cache) || !aligned16(Lw->v_cache) || !aligned16(ws))
+    return SWIFTSPEC_MISALIGNED;
+  const LayerWs w = layer_ws(d, T);
+  if (ws_bytes < w.total) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  char* base = static_cast<char*>(ws);
+  uint16_t* xn = reinterpret_cast<uint16_t*>(base + w.xn);
+  uint16_t* qkv = reinterpret_cast<uint16_t*>(base + w.qkv);
+  uint16_t* o = reinterpret_cast<uint16_t*>(base + w.o);
+  uint16_t* h = reinterpret_cast<uint16_t*>(base + w.h);
+  uint16_t* hn = reinterpret_cast<uint16_t*>(base + w.hn);
+  uint16_t* m = reinterpret_cast<uint16_t*>(base + w.m);
+  float* part = reinterpret_cast<float*>(base + w.part);
+  hipStream_t st = S(stream);
+  ss::launch_rmsnorm(hidden, T, H, H, Lw->attn_norm, d->eps, xn, H, st);
+  run_gemm(&Lw->wqkv, nullptr, xn, T, H, qkv, Nqkv, nullptr, 0, ws, part, st);
+  run_attention(qkv, Nqkv, qkv + Hd, qkv + Hd + d->Hkv * d->D, Nqkv, Lw->k_cache, Lw->v_cache,
+                d->S_max, d_prefix_len, d_parent, T, d->Hq, d->Hkv, d->D, rope,
+                1.0f / std::sqrt((float)d->D), o, Hd, ws, part, st);
+  run_gemm(&Lw->wo, nullptr, o, T, Hd, h, H, hidden, H, ws, part, st);
+  ss::launch_rmsnorm(h, T, H, H, Lw->mlp_norm, d->eps, hn, H, st);
+  run_gemm(&Lw->wgate, &Lw->wup, hn, T, H, m, F, nullptr, 0, ws, part, st);
+  run_gemm(&Lw->wdown, nullptr, m, T, F, hidden, H, h, H, ws, part, st);
+  return check_launch();
+}
+
+size_t swiftspec_lm_head_workspace_bytes(int32_t M, int32_t H, int32_t V) {
+  (void)M;
+  (void)H;
+  (void)V;
+  return kHeader;
+}
+
+int swiftspec_lm_head(const uint16_t* h, int32_t M, int32_t H, const uint16_t* gamma, float eps,
+                      const uint16_t* W, int32_t V, uint16_t* logits, void* ws, size_t ws_bytes,
+                      void* stream) {
+  (void)h; (void)M; (void)H; (void)gamma; (void)eps; (void)W; (void)V; (void)logits; (void)ws;
+  (void)ws_bytes; (void)stream;
+  return SWIFTSPEC_UNSUPPORTED;
+}
+
+struct swiftspec_graph {
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+};
+
+int swiftspec_graph_begin(void* stream) {
+  if (!stream) return SWIFTSPEC_INVALID_ARG;
+  return hip_status(hipStreamBeginCapture(S(stream), hipStreamCaptureModeThreadLocal));
+}
+
+int swiftspec_graph_end(void* stream, swiftspec_graph** out) {
+  if (!stream || !out) return SWIFTSPEC_INVALID_ARG;
+  hipGraph_t g = nullptr;
+  int rc = hip_status(hipStreamEndCapture(S(stream), &g));
+  if (rc) return rc;
+  hipGraphExec_t ex = nullptr;
+  rc = hip_status(hipGraphInstantiate(&ex, g, nullptr, nullptr, 0));
+  if (rc) {
+    (void)hipGraphDestroy(g);
+    return rc;
+  }
+  swiftspec_graph* r = new (std::nothrow) swiftspec_graph{g, ex};
+  if (!r) {
+    (void)hipGraphExecDestroy(ex);
+    (void)hipGraphDestroy(g);
+    return SWIFTSPEC_INVALID_ARG;
+  }
+  *out = r;
+  return SWIFTSPEC_OK;
+}
+
+int swiftspec_graph_launch(swiftspec_graph* g, void* stream) {
+  if (!g) return SWIFTSPEC_INVALID_ARG;
+  return hip_status(hipGraphLaunch(g->exec, S(stream)));
+}
+
+int swiftspec_graph_destroy(swiftspec_graph* g) {
+  if (!g) return SWIFTSPEC_INVALID_ARG;
+  (void)hipGraphExecDestroy(g->exec);
+  (void)hipGraphDestroy(g->graph);
+  delete g;
+  return SWIFTSPEC_OK;
+}
+
+}  // extern "C"

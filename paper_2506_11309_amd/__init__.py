@@ -41,7 +41,7 @@ class SwiftSpecError(RuntimeError):
 
 
 class W4(ctypes.Structure):
-    _fields_ = [("qweight", vp), ("scales", vp), ("zeros", vp), ("K", i32), ("N", i32)]
+    _fields_ = [("qweight", vp), ("scales", vp), ("zeros", vp), ("K", i32), ("N", i32), ("packed", vp)]
 
 
 class Dims(ctypes.Structure):
@@ -59,11 +59,18 @@ _SIGS = {
     "swiftspec_last_hip_error": ([], ctypes.c_int),
     "swiftspec_workspace_init": ([vp, sz, vp], ctypes.c_int),
     "swiftspec_read_device_error": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
+    "swiftspec_w4_packed_bytes": ([i32, i32], sz),
+    "swiftspec_w4_prepack": ([ctypes.POINTER(W4), vp, sz, vp], ctypes.c_int),
     "swiftspec_w4a16_gemm": ([ctypes.POINTER(W4), vp, i32, i32, vp, i32, vp, i32, vp, sz, vp], ctypes.c_int),
     "swiftspec_w4a16_gemm_workspace_bytes": ([i32, i32, i32], sz),
     "swiftspec_w4a16_swiglu": ([ctypes.POINTER(W4), ctypes.POINTER(W4), vp, i32, i32, vp, i32, vp, sz, vp],
                                ctypes.c_int),
     "swiftspec_w4a16_swiglu_workspace_bytes": ([i32, i32, i32], sz),
+    "swiftspec_prepared_bytes": ([i32, i32], sz),
+    "swiftspec_prepare_activations": ([vp, i32, i32, i32, vp, vp], ctypes.c_int),
+    "swiftspec_w4a16_gemm_prepared": ([ctypes.POINTER(W4), vp, i32, vp, i32, vp, i32, vp, sz, vp], ctypes.c_int),
+    "swiftspec_w4a16_swiglu_prepared": ([ctypes.POINTER(W4), ctypes.POINTER(W4), vp, i32, vp, i32, vp, sz, vp],
+                                        ctypes.c_int),
     "swiftspec_rmsnorm": ([vp, i32, i32, i32, vp, f32, vp, i32, vp], ctypes.c_int),
     "swiftspec_tree_attention": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, f32,
                                   vp, i32, vp, sz, vp], ctypes.c_int),
@@ -130,11 +137,27 @@ def workspace(nbytes: int, device="cuda"):
     return torch.zeros(int(nbytes), dtype=torch.uint8, device=device)
 
 
-def make_w4(qweight, scales, zeros) -> W4:
+def make_w4(qweight, scales, zeros, packed=None) -> W4:
     """Describe an int4 matrix held in device tensors qweight [N][K/2] u8,
-    scales [N][K/128] fp16, zeros [N][K/128] u8."""
+    scales [N][K/128] fp16, zeros [N][K/128] u8, and optionally its
+    kernel-native copy `packed` (see prepack_w4)."""
     N, half_k = qweight.shape
-    return W4(qweight.data_ptr(), scales.data_ptr(), zeros.data_ptr(), 2 * half_k, N)
+    return W4(qweight.data_ptr(), scales.data_ptr(), zeros.data_ptr(), 2 * half_k, N,
+              packed.data_ptr() if packed is not None else None)
+
+
+def packed_bytes(K: int, N: int) -> int:
+    return int(_load().swiftspec_w4_packed_bytes(K, N))
+
+
+def prepack_w4(W: W4, stream=None):
+    """Allocate and fill the kernel-native copy of W; returns the uint8
+    device tensor and sets W.packed to it (keep the tensor alive)."""
+    import torch
+    t = torch.empty(packed_bytes(W.K, W.N), dtype=torch.uint8, device="cuda")
+    _check(_load().swiftspec_w4_prepack(ctypes.byref(W), _ptr(t), t.numel(), _stream(stream)), "w4_prepack")
+    W.packed = t.data_ptr()
+    return t
 
 
 def rope_table(theta: float, S_max: int, D: int):
@@ -187,6 +210,30 @@ def w4a16_swiglu(Wg: W4, Wu: W4, x, y, ws, stream=None):
                                         x.stride(0), _ptr(y), y.stride(0), _ptr(ws), ws.numel(),
                                         _stream(stream))
     _check(st, "w4a16_swiglu")
+
+
+def prepared_bytes(M: int, K: int) -> int:
+    return int(_load().swiftspec_prepared_bytes(M, K))
+
+
+def prepare_activations(x, xp, stream=None):
+    """x [M][>=K] fp16 -> xp (uint8/int16 device buffer of prepared_bytes(M, K))."""
+    M, K = x.shape
+    _check(_load().swiftspec_prepare_activations(_ptr(x), M, x.stride(0), K, _ptr(xp), _stream(stream)),
+           "prepare_activations")
+
+
+def w4a16_gemm_prepared(W: W4, xp, M: int, y, ws, residual=None, stream=None):
+    st = _load().swiftspec_w4a16_gemm_prepared(ctypes.byref(W), _ptr(xp), M, _ptr(y), y.stride(0),
+                                               _ptr(residual), residual.stride(0) if residual is not None else 0,
+                                               _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "w4a16_gemm_prepared")
+
+
+def w4a16_swiglu_prepared(Wg: W4, Wu: W4, xp, M: int, y, ws, stream=None):
+    st = _load().swiftspec_w4a16_swiglu_prepared(ctypes.byref(Wg), ctypes.byref(Wu), _ptr(xp), M, _ptr(y),
+                                                 y.stride(0), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "w4a16_swiglu_prepared")
 
 
 def rmsnorm(x, gamma, out, eps=1e-5, stream=None):

@@ -9,7 +9,8 @@ namespace ss {
 // fp32 sum of squares, fixed reduction order (deterministic).
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x, int H, int ldx,
                                                       const uint16_t* __restrict__ gamma, float eps,
-                                                      uint16_t* __restrict__ out, int ldo) {
+                                                      uint16_t* __restrict__ out, int ldo,
+                                                      uint16_t* __restrict__ out_prep) {
   __shared__ float partial[4];
   const int m = blockIdx.x;
   const uint16_t* xr = x + (size_t)m * ldx;
@@ -36,12 +37,18 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[e] = (_Float16)(((float)h[e] * inv) * (float)gm[e]);
     *reinterpret_cast<u32x4*>(orow + c) = bitcast<u32x4>(o);
+    if (out_prep) {
+      const u32x4 ob = bitcast<u32x4>(o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        store_prepared(out_prep, m, c + e, H >> 7, (uint16_t)(ob[e >> 1] >> (16 * (e & 1))));
+    }
   }
 }
 
 void launch_rmsnorm(const uint16_t* x, int M, int H, int ldx, const uint16_t* gamma, float eps,
-                    uint16_t* out, int ldo, hipStream_t st) {
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo);
+                    uint16_t* out, int ldo, uint16_t* out_prep, hipStream_t st) {
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo, out_prep);
 }
 
 // ---------------------------------------------------------------- KV commit

@@ -127,3 +127,38 @@ __device__ __forceinline__ void reset_counter(uint32_t* counter) {
 }
 
 }  // namespace ss
+
+namespace ss {
+
+// ---- activation layout consumed by the W4A16 GEMMs ("prepared" layout) ----
+// For a GEMM input x[M][K] with G = K / 128 quantisation groups, the matrix
+// is stored as [M/16 tiles][G][4 fragments][64 lanes][8] fp16 so that a wave
+// fetches each MFMA A-fragment with one coalesced 16-byte load per lane.
+// Lane kq*16 + (m % 16) of fragment f holds 8 values of row m from k-range
+// [128 g + 32 kq, +32), in the slot order the int4 dequantisation produces:
+// fragments 0/1 take the even k of that range (first/second 16), stored
+// multiplied by 16 (exact), fragments 2/3 the odd k.  Within a fragment the
+// order is 0,4,2,6,8,12,10,14 (+1 for odd k).
+__host__ __device__ inline size_t prep_offset(int m, int k, int G, bool* lo) {
+  const int mt = m >> 4, r16 = m & 15, g = k >> 7, j = k & 127, kq = j >> 5, t = j & 31;
+  const int f = ((t & 1) << 1) | (t >> 4);
+  const int u = (t & 15) >> 1;
+  const int e = (u & 4) | ((u & 1) << 1) | ((u >> 1) & 1);
+  *lo = (t & 1) == 0;
+  return ((((size_t)mt * G + g) * 4 + f) * 64 + (kq * 16 + r16)) * 8 + e;
+}
+
+// Store the fp16 value h of activation (m, k) into a prepared buffer.
+__device__ __forceinline__ void store_prepared(uint16_t* prep, int m, int k, int G, uint16_t h) {
+  bool lo;
+  const size_t off = prep_offset(m, k, G, &lo);
+  if (lo) {
+    _Float16 v;
+    __builtin_memcpy(&v, &h, 2);
+    v = v * (_Float16)16.0f;  // exact scaling by a power of two
+    __builtin_memcpy(&h, &v, 2);
+  }
+  prep[off] = h;
+}
+
+}  // namespace ss

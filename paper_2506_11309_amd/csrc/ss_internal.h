@@ -8,35 +8,39 @@
 
 namespace ss {
 
-struct W4Host {
-  const uint8_t* q;
-  const uint16_t* s;
-  const uint8_t* z;
-};
+// Fixed grid of the stream-K GEMMs: two 4-wave workgroups per CU of MI355X.
+constexpr int kGemmWorkgroups = 512;
 
 struct GemmLaunch {
-  W4Host w0, w1;  // w1: up-projection of the fused SwiGLU
+  const void* w0;  // kernel-native (prepacked) weights
+  const void* w1;  // up-projection of the fused SwiGLU
   int K, N;       // N = output columns
-  const uint16_t* x;
-  int M, ldx;
-  uint16_t* y;
+  const uint16_t* aprep;  // activations in the prepared layout
+  int M;
+  uint16_t* y;      // plain output (nullable)
   int ldy;
+  uint16_t* yprep;  // prepared output for a following GEMM (nullable)
   const uint16_t* res;
   int ldr;
-  int nw;       // N-tiles (16 columns) per workgroup, counting gate and up tiles for SwiGLU
+  int nw;       // N-tiles (16 columns) per block, counting gate and up tiles for SwiGLU
   int nblocks;  // column blocks
-  int nsplit;   // K-splits
+  int nwg;      // workgroups launched
   bool swiglu;
   float* part;
   uint32_t* counters;
 };
 
 struct GemmPlan {
-  int nw, nblocks, nsplit;
-  size_t part_bytes;
+  int nw, nblocks, nwg;
+  size_t part_bytes;  // split partials
+  size_t prep_bytes;  // prepared activations of the input
 };
 GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu);
 void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st);
+void launch_prepare_activations(const uint16_t* x, int M, int ldx, int K, uint16_t* out, hipStream_t st);
+void launch_prepack_w4(const uint8_t* q, const uint16_t* s, const uint8_t* z, int K, int N, void* packed,
+                       hipStream_t st);
+inline size_t w4_packed_bytes(int K, int N) { return (size_t)K * N / 2 + (size_t)N * (K / 128) * 4; }
 
 struct DenseGemmLaunch {
   const uint16_t* w;  // [N][K] fp16
@@ -68,6 +72,7 @@ struct AttnLaunch {
   float scale;
   uint16_t* out;
   int ldo;
+  uint16_t* out_prep;  // attention output also in the prepared layout (nullable)
   void* ws;         // header (error word, counters)
   float* part;      // split partials
   int nsplit;       // key splits per kv head
@@ -81,7 +86,7 @@ AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max);
 void launch_tree_attention(const AttnLaunch& L, hipStream_t st);
 
 void launch_rmsnorm(const uint16_t* x, int M, int H, int ldx, const uint16_t* gamma, float eps,
-                    uint16_t* out, int ldo, hipStream_t st);
+                    uint16_t* out, int ldo, uint16_t* out_prep, hipStream_t st);
 
 void launch_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_t layer_stride,
                       int Hkv, int S_max, int D, int32_t* prefix_len, const int32_t* parent, int T,

@@ -38,11 +38,19 @@ int hip_status(hipError_t e) {
   return SWIFTSPEC_OK;
 }
 
-int check_w4(const swiftspec_w4* W) {
-  if (!W || !W->qweight || !W->scales || !W->zeros) return SWIFTSPEC_INVALID_ARG;
+int check_w4_shape(const swiftspec_w4* W) {
+  if (!W) return SWIFTSPEC_INVALID_ARG;
   if (W->K <= 0 || W->N <= 0) return SWIFTSPEC_INVALID_ARG;
-  if (W->K % 128 != 0 || W->N % 16 != 0) return SWIFTSPEC_UNSUPPORTED;
-  if (!aligned16(W->qweight)) return SWIFTSPEC_MISALIGNED;
+  if (W->K % 128 != 0 || W->N % 64 != 0) return SWIFTSPEC_UNSUPPORTED;
+  return SWIFTSPEC_OK;
+}
+
+// The compute entry points read the kernel-native copy only.
+int check_w4(const swiftspec_w4* W) {
+  int rc = check_w4_shape(W);
+  if (rc) return rc;
+  if (!W->packed) return SWIFTSPEC_INVALID_ARG;
+  if (!aligned16(W->packed)) return SWIFTSPEC_MISALIGNED;
   return SWIFTSPEC_OK;
 }
 
@@ -59,34 +67,45 @@ bool attn_counters_fit(int T, int Hq, int Hkv) {
 
 size_t gemm_ws(int M, int K, int N, bool swiglu) {
   ss::GemmPlan p = ss::plan_w4a16_gemm(M, K, N, swiglu);
-  return kHeader + align_up(p.part_bytes);
+  return kHeader + align_up(p.prep_bytes) + align_up(p.part_bytes);
 }
 
-// Launch a validated W4A16 GEMM / SwiGLU with partials in `part`.
-void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* x, int M, int ldx,
-              uint16_t* y, int ldy, const uint16_t* res, int ldr, void* ws, float* part,
-              hipStream_t st) {
+// Launch a validated W4A16 GEMM / SwiGLU reading prepared activations.
+void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* aprep, int M,
+              uint16_t* y, int ldy, uint16_t* yprep, const uint16_t* res, int ldr, void* ws,
+              float* part, hipStream_t st) {
   const bool swiglu = W1 != nullptr;
   ss::GemmPlan p = ss::plan_w4a16_gemm(M, W0->K, W0->N, swiglu);
   ss::GemmLaunch L;
-  L.w0 = {W0->qweight, W0->scales, W0->zeros};
-  L.w1 = swiglu ? ss::W4Host{W1->qweight, W1->scales, W1->zeros} : L.w0;
+  L.w0 = W0->packed;
+  L.w1 = swiglu ? W1->packed : W0->packed;
   L.K = W0->K;
   L.N = W0->N;
-  L.x = x;
+  L.aprep = aprep;
   L.M = M;
-  L.ldx = ldx;
   L.y = y;
   L.ldy = ldy;
+  L.yprep = yprep;
   L.res = res;
   L.ldr = ldr;
   L.nw = p.nw;
   L.nblocks = p.nblocks;
-  L.nsplit = p.nsplit;
+  L.nwg = p.nwg;
   L.swiglu = swiglu;
   L.part = part;
   L.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + 256);
   ss::launch_w4a16_gemm(L, st);
+}
+
+// Standalone entry: prepare plain x into the workspace, then run the GEMM.
+void run_gemm_plain(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* x, int M, int ldx,
+                    uint16_t* y, int ldy, const uint16_t* res, int ldr, void* ws, hipStream_t st) {
+  ss::GemmPlan p = ss::plan_w4a16_gemm(M, W0->K, W0->N, W1 != nullptr);
+  char* base = static_cast<char*>(ws);
+  uint16_t* aprep = reinterpret_cast<uint16_t*>(base + kHeader);
+  float* part = reinterpret_cast<float*>(base + kHeader + align_up(p.prep_bytes));
+  ss::launch_prepare_activations(x, M, ldx, W0->K, aprep, st);
+  run_gemm(W0, W1, aprep, M, y, ldy, nullptr, res, ldr, ws, part, st);
 }
 
 int check_tree_attention_args(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v,
@@ -112,7 +131,7 @@ size_t attn_ws(int T, int Hq, int Hkv, int D, int S_max) {
 void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v, int ldkv,
                    uint16_t* kc, uint16_t* vc, int S_max, const int32_t* P, const int32_t* parent,
                    int T, int Hq, int Hkv, int D, const float* rope, float scale, uint16_t* out,
-                   int ldo, void* ws, float* part, hipStream_t st) {
+                   int ldo, uint16_t* out_prep, void* ws, float* part, hipStream_t st) {
   ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max);
   ss::AttnLaunch L;
   L.q = q;
@@ -133,6 +152,7 @@ void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t
   L.scale = scale;
   L.out = out;
   L.ldo = ldo;
+  L.out_prep = out_prep;
   L.ws = ws;
   L.part = part;
   L.nsplit = p.nsplit;
@@ -141,25 +161,29 @@ void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t
 }
 
 struct LayerWs {
-  size_t xn, qkv, o, h, hn, m, part, total;
+  size_t xn, qkv, o, h, hn, m, xn_p, o_p, hn_p, m_p, part, total;
 };
 
 LayerWs layer_ws(const swiftspec_dims* d, int T) {
   LayerWs w;
   const int Nqkv = (d->Hq + 2 * d->Hkv) * d->D;
+  const size_t MT16 = (size_t)((T + 15) / 16) * 16;  // prepared buffers hold whole 16-row tiles
   size_t off = kHeader;
-  w.xn = off;
-  off += align_up((size_t)T * d->H * 2);
-  w.qkv = off;
-  off += align_up((size_t)T * Nqkv * 2);
-  w.o = off;
-  off += align_up((size_t)T * d->Hq * d->D * 2);
-  w.h = off;
-  off += align_up((size_t)T * d->H * 2);
-  w.hn = off;
-  off += align_up((size_t)T * d->H * 2);
-  w.m = off;
-  off += align_up((size_t)T * d->F * 2);
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  w.xn = take((size_t)T * d->H * 2);
+  w.qkv = take((size_t)T * Nqkv * 2);
+  w.o = take((size_t)T * d->Hq * d->D * 2);
+  w.h = take((size_t)T * d->H * 2);
+  w.hn = take((size_t)T * d->H * 2);
+  w.m = take((size_t)T * d->F * 2);
+  w.xn_p = take(MT16 * d->H * 2);
+  w.o_p = take(MT16 * d->Hq * d->D * 2);
+  w.hn_p = take(MT16 * d->H * 2);
+  w.m_p = take(MT16 * d->F * 2);
   size_t part = 0;
   auto upd = [&](size_t b) { part = b > part ? b : part; };
   upd(ss::plan_w4a16_gemm(T, d->H, Nqkv, false).part_bytes);
@@ -167,8 +191,7 @@ LayerWs layer_ws(const swiftspec_dims* d, int T) {
   upd(ss::plan_w4a16_gemm(T, d->H, d->F, true).part_bytes);
   upd(ss::plan_w4a16_gemm(T, d->F, d->H, false).part_bytes);
   upd(ss::plan_tree_attention(T, d->Hq, d->Hkv, d->D, d->S_max).part_bytes);
-  w.part = off;
-  off += align_up(part);
+  w.part = take(part);
   w.total = off;
   return w;
 }
@@ -210,6 +233,21 @@ int swiftspec_read_device_error(void* ws, void* stream, uint32_t* out) {
   return hip_status(hipStreamSynchronize(S(stream)));
 }
 
+size_t swiftspec_w4_packed_bytes(int32_t K, int32_t N) {
+  if (K <= 0 || N <= 0) return 0;
+  return ss::w4_packed_bytes(K, N);
+}
+
+int swiftspec_w4_prepack(const swiftspec_w4* W, void* packed, size_t packed_bytes, void* stream) {
+  int rc = check_w4_shape(W);
+  if (rc) return rc;
+  if (!W->qweight || !W->scales || !W->zeros || !packed) return SWIFTSPEC_INVALID_ARG;
+  if (!aligned16(W->qweight) || !aligned16(packed)) return SWIFTSPEC_MISALIGNED;
+  if (packed_bytes < ss::w4_packed_bytes(W->K, W->N)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  ss::launch_prepack_w4(W->qweight, W->scales, W->zeros, W->K, W->N, packed, S(stream));
+  return check_launch();
+}
+
 size_t swiftspec_w4a16_gemm_workspace_bytes(int32_t M, int32_t K, int32_t N) {
   if (M < 1 || K < 128 || N < 16) return kHeader;
   return gemm_ws(M, K, N, false);
@@ -233,8 +271,7 @@ int swiftspec_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, in
   if (M == 0) return SWIFTSPEC_OK;
   if (!gemm_counters_fit(M, W->K, W->N, false)) return SWIFTSPEC_UNSUPPORTED;
   if (ws_bytes < gemm_ws(M, W->K, W->N, false)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
-  run_gemm(W, nullptr, x, M, ldx, y, ldy, residual, ldr, ws,
-           reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
+  run_gemm_plain(W, nullptr, x, M, ldx, y, ldy, residual, ldr, ws, S(stream));
   return check_launch();
 }
 
@@ -253,7 +290,59 @@ int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const
   if (M == 0) return SWIFTSPEC_OK;
   if (!gemm_counters_fit(M, Wg->K, Wg->N, true)) return SWIFTSPEC_UNSUPPORTED;
   if (ws_bytes < gemm_ws(M, Wg->K, Wg->N, true)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
-  run_gemm(Wg, Wu, x, M, ldx, y, ldy, nullptr, 0, ws,
+  run_gemm_plain(Wg, Wu, x, M, ldx, y, ldy, nullptr, 0, ws, S(stream));
+  return check_launch();
+}
+
+size_t swiftspec_prepared_bytes(int32_t M, int32_t K) {
+  if (M < 1 || K < 128 || K % 128) return 0;
+  return (size_t)((M + 15) / 16) * (K / 128) * 4 * 64 * 16;
+}
+
+int swiftspec_prepare_activations(const uint16_t* x, int32_t M, int32_t ldx, int32_t K, uint16_t* xp,
+                                  void* stream) {
+  if (!x || !xp || M < 0 || K <= 0 || ldx < K) return SWIFTSPEC_INVALID_ARG;
+  if (K % 128 || M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(xp) || ldx % 8) return SWIFTSPEC_MISALIGNED;
+  if (M == 0) return SWIFTSPEC_OK;
+  ss::launch_prepare_activations(x, M, ldx, K, xp, S(stream));
+  return check_launch();
+}
+
+int swiftspec_w4a16_gemm_prepared(const swiftspec_w4* W, const uint16_t* xp, int32_t M, uint16_t* y,
+                                  int32_t ldy, const uint16_t* residual, int32_t ldr, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  int rc = check_w4(W);
+  if (rc) return rc;
+  if (!xp || !y || !ws || M < 0 || ldy < W->N || (residual && ldr < W->N)) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(xp)) return SWIFTSPEC_MISALIGNED;
+  if (residual == y && ldr != ldy) return SWIFTSPEC_INVALID_ARG;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (!gemm_counters_fit(M, W->K, W->N, false)) return SWIFTSPEC_UNSUPPORTED;
+  ss::GemmPlan p = ss::plan_w4a16_gemm(M, W->K, W->N, false);
+  if (ws_bytes < kHeader + align_up(p.part_bytes)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  run_gemm(W, nullptr, xp, M, y, ldy, nullptr, residual, ldr, ws,
+           reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
+  return check_launch();
+}
+
+int swiftspec_w4a16_swiglu_prepared(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* xp,
+                                    int32_t M, uint16_t* y, int32_t ldy, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  int rc = check_w4(Wg);
+  if (rc) return rc;
+  rc = check_w4(Wu);
+  if (rc) return rc;
+  if (Wg->K != Wu->K || Wg->N != Wu->N) return SWIFTSPEC_INVALID_ARG;
+  if (!xp || !y || !ws || M < 0 || ldy < Wg->N) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(xp)) return SWIFTSPEC_MISALIGNED;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (!gemm_counters_fit(M, Wg->K, Wg->N, true)) return SWIFTSPEC_UNSUPPORTED;
+  ss::GemmPlan p = ss::plan_w4a16_gemm(M, Wg->K, Wg->N, true);
+  if (ws_bytes < kHeader + align_up(p.part_bytes)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  run_gemm(Wg, Wu, xp, M, y, ldy, nullptr, nullptr, 0, ws,
            reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
   return check_launch();
 }
@@ -265,7 +354,7 @@ int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, cons
   if (!aligned16(x) || !aligned16(gamma) || !aligned16(out) || ldx % 8 || ldo % 8)
     return SWIFTSPEC_MISALIGNED;
   if (M == 0) return SWIFTSPEC_OK;
-  ss::launch_rmsnorm(x, M, H, ldx, gamma, eps, out, ldo, S(stream));
+  ss::launch_rmsnorm(x, M, H, ldx, gamma, eps, out, ldo, nullptr, S(stream));
   return check_launch();
 }
 
@@ -287,7 +376,7 @@ int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, 
   if (!ws) return SWIFTSPEC_INVALID_ARG;
   if (ws_bytes < attn_ws(T, Hq, Hkv, D, S_max)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   run_attention(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_parent, T, Hq, Hkv, D,
-                rope_cos_sin, softmax_scale, out, ldo, ws,
+                rope_cos_sin, softmax_scale, out, ldo, nullptr, ws,
                 reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
   return check_launch();
 }
@@ -386,23 +475,20 @@ int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, u
   const LayerWs w = layer_ws(d, T);
   if (ws_bytes < w.total) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   char* base = static_cast<char*>(ws);
-  uint16_t* xn = reinterpret_cast<uint16_t*>(base + w.xn);
-  uint16_t* qkv = reinterpret_cast<uint16_t*>(base + w.qkv);
-  uint16_t* o = reinterpret_cast<uint16_t*>(base + w.o);
-  uint16_t* h = reinterpret_cast<uint16_t*>(base + w.h);
-  uint16_t* hn = reinterpret_cast<uint16_t*>(base + w.hn);
-  uint16_t* m = reinterpret_cast<uint16_t*>(base + w.m);
+  auto at = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
+  uint16_t *xn = at(w.xn), *qkv = at(w.qkv), *o = at(w.o), *h = at(w.h), *hn = at(w.hn), *m = at(w.m);
+  uint16_t *xn_p = at(w.xn_p), *o_p = at(w.o_p), *hn_p = at(w.hn_p), *m_p = at(w.m_p);
   float* part = reinterpret_cast<float*>(base + w.part);
   hipStream_t st = S(stream);
-  ss::launch_rmsnorm(hidden, T, H, H, Lw->attn_norm, d->eps, xn, H, st);
-  run_gemm(&Lw->wqkv, nullptr, xn, T, H, qkv, Nqkv, nullptr, 0, ws, part, st);
+  ss::launch_rmsnorm(hidden, T, H, H, Lw->attn_norm, d->eps, xn, H, xn_p, st);
+  run_gemm(&Lw->wqkv, nullptr, xn_p, T, qkv, Nqkv, nullptr, nullptr, 0, ws, part, st);
   run_attention(qkv, Nqkv, qkv + Hd, qkv + Hd + d->Hkv * d->D, Nqkv, Lw->k_cache, Lw->v_cache,
                 d->S_max, d_prefix_len, d_parent, T, d->Hq, d->Hkv, d->D, rope,
-                1.0f / std::sqrt((float)d->D), o, Hd, ws, part, st);
-  run_gemm(&Lw->wo, nullptr, o, T, Hd, h, H, hidden, H, ws, part, st);
-  ss::launch_rmsnorm(h, T, H, H, Lw->mlp_norm, d->eps, hn, H, st);
-  run_gemm(&Lw->wgate, &Lw->wup, hn, T, H, m, F, nullptr, 0, ws, part, st);
-  run_gemm(&Lw->wdown, nullptr, m, T, F, hidden, H, h, H, ws, part, st);
+                1.0f / std::sqrt((float)d->D), o, Hd, o_p, ws, part, st);
+  run_gemm(&Lw->wo, nullptr, o_p, T, h, H, nullptr, hidden, H, ws, part, st);
+  ss::launch_rmsnorm(h, T, H, H, Lw->mlp_norm, d->eps, hn, H, hn_p, st);
+  run_gemm(&Lw->wgate, &Lw->wup, hn_p, T, m, F, m_p, nullptr, 0, ws, part, st);
+  run_gemm(&Lw->wdown, nullptr, m_p, T, hidden, H, nullptr, h, H, ws, part, st);
   return check_launch();
 }
 

@@ -37,6 +37,7 @@ struct AttnArgs {
   const int32_t* parent;
   const float* rope;
   uint16_t* out;
+  uint16_t* out_prep;
   void* ws;
   float* part;
   int ldq, ldkv, ldo, S_max, T, Hq, Hkv, G, R, RB, nsplit;
@@ -348,7 +349,11 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
       const float inv = 1.0f / lsum[r];
       uint16_t* dst = a.out + (size_t)i * a.ldo + qh * D;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + n16] = f2h(acc[dt][r] * inv);
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint16_t h = f2h(acc[dt][r] * inv);
+        dst[dt * 16 + n16] = h;
+        if (a.out_prep) store_prepared(a.out_prep, i, qh * D + dt * 16 + n16, (a.Hq * D) >> 7, h);
+      }
     }
   }
 }
@@ -382,6 +387,7 @@ void launch_tree_attention(const AttnLaunch& L, hipStream_t st) {
   a.parent = L.parent;
   a.rope = L.rope;
   a.out = L.out;
+  a.out_prep = L.out_prep;
   a.ws = L.ws;
   a.part = L.part;
   a.ldq = L.ldq;

@@ -1,311 +1,432 @@
 // W4A16 GEMMs at small M (the tree size) for gfx950.
 //
-// y[m][n] = sum_k x[m][k] * W'[n][k], W'[n][k] = (q[n][k] - z[n][g]) * s[n][g],
-// g = k / 128: the int4 AWQ-style projections of a decoder layer
-// (SwiftSpec Sec. 3.3 and Sec. 5.1).  Variants: plain (+ residual), fused
-// SwiGLU (gate and up tiles share the activation fragments, Sec. 3.3), and
-// a dense fp16-weight variant for the LM head.
+// y[m][n] = sum_k x[m][k] * W'[n][k],  W'[n][k] = (q[n][k] - z[n][g]) * s[n][g],
+// g = k / 128: the int4 AWQ-style projections of a decoder layer (SwiftSpec
+// Sec. 3.3 and Sec. 5.1), plain (+ residual) or as the fused SwiGLU whose
+// gate and up tiles share the activation fragments (Sec. 3.3).
 //
-// Mapping onto the matrix cores (v_mfma_f32_16x16x32_f16, wave64):
-//   * A operand = activations, 16 token rows per M-tile (rows >= M are zero);
-//     B operand = weights, 16 output columns per N-tile.
-//   * One 16-byte load per lane fetches 32 consecutive k of one weight row:
-//     lane (n = lane % 16, kq = lane / 16) reads k in [32 kq, 32 kq + 32) of
-//     a 128-wide quantisation group, so one wave-wide load covers exactly a
-//     16 x 128 (column x group) block and one (scale, zero) pair per lane.
-//   * Dequantisation in registers without shifts of the high nibbles:
-//       (w & 0x000F000F) | 0x64006400  = fp16 pair (1024 + q_lo, ...)
-//       (w & 0x00F000F0) | 0x64006400  = fp16 pair (1024 + 16 q_hi, ...)
-//     followed by one packed fp16 subtraction of (1024 + z) resp.
-//     (1024 + 16 z), both exact.  Low-nibble k slots are matched with
-//     activations pre-multiplied by 16 (exact in fp16), so every product is
-//     16 x (q - z); the group sum is scaled by s / 16 in fp32.  The k-slot
-//     order inside an MFMA is a permutation of the group's k, applied
-//     identically to both operands.
-//   * Each workgroup (4 waves) owns NW N-tiles for one K-split; its waves
-//     take interleaved quantisation groups (so together they stream 256
-//     contiguous bytes of every weight row), and reduce through LDS.
-//   * K-splits of one N-block are combined by the last-arriving workgroup
-//     (atomic ticket) in split order, so the result is deterministic.
-//     Partials use agent-scope coherent 8-byte stores/loads; blockIdx is
-//     laid out so all splits of an N-block share blockIdx % 8 (one XCD when
-//     workgroups are dispatched round-robin over the 8 XCDs).
+// Matrix-core mapping (v_mfma_f32_16x16x32_f16, wave64):
+//   * A operand = activations in the "prepared" layout (ss_device.h), 16
+//     token rows per M-tile; B operand = weights, 16 output columns per
+//     N-tile.  Rows >= M are zero.
+//   * Lane (n = lane % 16, kq = lane / 16) loads 16 bytes = k in
+//     [128 g + 32 kq, +32) of weight row n: one wave-wide load covers one
+//     16-column x 128-k block, i.e. exactly one (scale, zero) group.
+//   * Dequantisation by masking only: (w & 0x000F000F) is the fp16 pair
+//     (q * 2^-24, q' * 2^-24) (subnormals, which the matrix cores take
+//     exactly) and (w & 0x00F000F0) is (16 q * 2^-24, ...).  Low-nibble slots
+//     meet activations pre-multiplied by 16, so every product is
+//     x * q * 2^-20 exactly and the MFMA sum of a group is
+//     C_g = 2^-20 sum_k x q.  The zero point is applied through the row sums
+//     S_g[m] = sum_k x[m][k] of the group (four more MFMAs against constant
+//     B fragments, landing directly in the accumulator layout):
+//         y += s * 2^20 * C_g - (s * z) * S_g.
+//   * Stream-K scheduling: a fixed grid of workgroups (4 waves each) splits
+//     the (N-block, group) iteration space into equal contiguous ranges.
+//     Inside a range, the waves take interleaved groups of the same N-block
+//     (together they stream 256 contiguous bytes of every weight row), run a
+//     3-stage register pipeline (loads for group i+2 in flight while group i
+//     computes), and reduce through LDS.  An N-block split between
+//     workgroups is finished by the last contributor to arrive (atomic
+//     ticket), which sums the partials in a fixed order: results are
+//     deterministic.  Partials use agent-scope coherent stores/loads.
+//     Consecutive ranges are placed on the same XCD (blockIdx % 8 selects
+//     the XCD under round-robin dispatch) so split N-blocks stay on one L2.
 #include "ss_device.h"
 #include "ss_internal.h"
 
 namespace ss {
 
-struct W4Ptr {
-  const uint8_t* q;
-  const uint16_t* s;
-  const uint8_t* z;
-};
-
 enum { EPI_PLAIN = 0, EPI_SWIGLU = 1 };
 
-__device__ __forceinline__ uint32_t pk_lo(uint32_t u, uint32_t v) { return (u & 0xFFFFu) | (v << 16); }
-__device__ __forceinline__ uint32_t pk_hi(uint32_t u, uint32_t v) { return (u >> 16) | (v & 0xFFFF0000u); }
+// Kernel-native copy of an int4 matrix (written by prepack_w4_kernel):
+//   q : [N/16 tiles][G groups][64 lanes] x 16 bytes -- lane kq*16 + c holds
+//       the packed nibbles of k in [128 g + 32 kq, +32) of row 16 t + c, in
+//       the original byte order; one wave-wide load is 1 KB contiguous and a
+//       tile's groups follow each other;
+//   sz: [N/16][G][16] x u32 -- scale (fp16 bits) | zero << 16 of row 16 t + c.
+struct W4Ptr {
+  const u32x4* q;
+  const uint32_t* sz;
+};
 
-// Activation fragments of one 16-row M-tile for one group, from 32
-// consecutive fp16 of the lane's row (a[0..15] = pairs (x_2j, x_2j+1)).
-// frag[0] / frag[1]: low-nibble slots of k 0..15 / 16..31, times 16;
-// frag[2] / frag[3]: high-nibble slots.
-__device__ __forceinline__ void act_fragments(const u32x4 raw[4], half8 frag[4]) {
-  uint32_t a[16];
+struct GemmArgs {
+  W4Ptr w0, w1;
+  int K, N, G;
+  const uint16_t* a;  // prepared activations [MT][G][4][64][8]
+  int M;
+  uint16_t* y;        // plain output [M][ldy] (nullable)
+  int ldy;
+  uint16_t* yp;       // prepared output for a following GEMM with K = N (nullable)
+  const uint16_t* res;
+  int ldr;
+  int nblocks, nwg;
+  long units;
+  float* part;
+  uint32_t* counters;
+};
+
+__device__ __forceinline__ long range_begin(long units, int v, int nwg) { return units * v / nwg; }
+
+template <int MT, int NWV>
+struct BStage {
+  u32x4 b[NWV];
+  uint32_t sz[NWV];
+};
+
+// Row sums of one group's activations, in accumulator layout: MFMA against
+// constant B fragments (1/16 for the x16-scaled low-nibble slots, 1 else).
+template <int MT>
+__device__ __forceinline__ void group_row_sums(const u32x4 (*frag)[4][kWave], f32x4* out, int lane) {
+  const half8 one16 = {(_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f,
+                       (_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f};
+  const half8 one = {(_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f,
+                     (_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    a[4 * i + 0] = raw[i][0];
-    a[4 * i + 1] = raw[i][1];
-    a[4 * i + 2] = raw[i][2];
-    a[4 * i + 3] = raw[i][3];
+  for (int mt = 0; mt < MT; ++mt) {
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(frag[mt][0][lane]), one16, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(frag[mt][1][lane]), one16, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(frag[mt][2][lane]), one, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(frag[mt][3][lane]), one, c, 0, 0, 0);
+    out[mt] = c;
+  }
+}
+
+constexpr int kRingB = 6;  // weight register ring: loads run 5 groups ahead
+constexpr int kRingA = 3;  // activation LDS ring
+
+template <int MT, int NWV, int EPI>
+__global__ __launch_bounds__(256) void w4a16_gemm_kernel(GemmArgs a) {
+  constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;  // output column tiles per wave
+  constexpr int kColB = 4 * kColW;                             // output column tiles per block
+  constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;
+  constexpr int kWaveSlotFloats = MT * kColW * kSrc * kWave * 4;
+  __shared__ u32x4 abuf[kRingA][MT][4][kWave];  // activation fragments of 3 groups
+  __shared__ f32x4 sxbuf[kRingA][MT][kWave];    // their row sums
+  __shared__ uint32_t s_ticket;
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int ncol = lane & 15;
+  const int kq = lane >> 4;
+  const int G = a.G;
+  const int b = blockIdx.x;
+  const int v = (a.nwg % 8 == 0) ? (b % 8) * (a.nwg / 8) + b / 8 : b;
+  const int u_lo = (int)range_begin(a.units, v, a.nwg), u_hi = (int)range_begin(a.units, v + 1, a.nwg);
+  const int total = u_hi - u_lo;
+  if (total <= 0) return;
+  const int st_f = tid >> 6;  // activation staging: fragment tid / 64 of every M-tile
+
+  // unit u = (N-block u / G, group u % G); index i counts units from u_lo (clamped)
+  auto unit_of = [&](int i) { return u_lo + (i < total ? i : total - 1); };
+  auto load_b = [&](int i, BStage<MT, NWV>& st) {
+    const int u = unit_of(i);
+    const int nb = u / G, g = u - nb * G;
+    const int tw = nb * kColB + wave * kColW;  // first column tile of this wave
+#pragma unroll
+    for (int nt = 0; nt < NWV; ++nt) {
+      const W4Ptr& w = (EPI == EPI_SWIGLU && nt >= kColW) ? a.w1 : a.w0;
+      const size_t tg = (size_t)(tw + nt % kColW) * G + g;
+      st.b[nt] = w.q[tg * kWave + lane];
+      st.sz[nt] = w.sz[tg * 16 + ncol];
+    }
+  };
+  auto load_a = [&](int i, u32x4 (&r)[MT]) {
+    const int g = unit_of(i) % G;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+      r[mt] = *reinterpret_cast<const u32x4*>(a.a + ((((size_t)mt * G + g) * 4 + st_f) * kWave + lane) * 8);
+  };
+  auto store_a = [&](int slot, const u32x4 (&r)[MT]) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) abuf[slot][mt][st_f][lane] = r[mt];
+  };
+  auto row_sums = [&](int slot) {
+    f32x4 s[MT];
+    group_row_sums<MT>(abuf[slot], s, lane);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) sxbuf[slot][mt][lane] = s[mt];
+  };
+
+  f32x4 acc[MT][NWV];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int slot, const BStage<MT, NWV>& st) {
+    half8 af[MT][4];
+    f32x4 sx[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+      for (int f = 0; f < 4; ++f) af[mt][f] = bitcast<half8>(abuf[slot][mt][f][lane]);
+      sx[mt] = sxbuf[slot][mt][lane];
+    }
+#pragma unroll
+    for (int nt = 0; nt < NWV; ++nt) {
+      const u32x4 w = st.b[nt];
+      const uint32_t s0 = w[0] >> 8, s1 = w[1] >> 8, s2 = w[2] >> 8, s3 = w[3] >> 8;
+      const half8 blo_a = bitcast<half8>(u32x4{w[0] & 0x000F000Fu, s0 & 0x000F000Fu, w[1] & 0x000F000Fu, s1 & 0x000F000Fu});
+      const half8 blo_b = bitcast<half8>(u32x4{w[2] & 0x000F000Fu, s2 & 0x000F000Fu, w[3] & 0x000F000Fu, s3 & 0x000F000Fu});
+      const half8 bhi_a = bitcast<half8>(u32x4{w[0] & 0x00F000F0u, s0 & 0x00F000F0u, w[1] & 0x00F000F0u, s1 & 0x00F000F0u});
+      const half8 bhi_b = bitcast<half8>(u32x4{w[2] & 0x00F000F0u, s2 & 0x00F000F0u, w[3] & 0x00F000F0u, s3 & 0x00F000F0u});
+      const float sc = h2f((uint16_t)(st.sz[nt] & 0xFFFFu));
+      const float s20 = sc * 1048576.0f;
+      const float nsz = -sc * (float)((st.sz[nt] >> 16) & 0xFFu);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 c = {0.f, 0.f, 0.f, 0.f};
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][0], blo_a, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][1], blo_b, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][2], bhi_a, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][3], bhi_b, c, 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          acc[mt][nt][r] = __builtin_fmaf(sx[mt][r], nsz, __builtin_fmaf(c[r], s20, acc[mt][nt][r]));
+      }
+    }
+  };
+
+  // End of an N-block's share: write the outputs (whole N-block in this
+  // range) or publish a partial and let the last contributor combine.
+  auto flush = [&](int nb) {
+    const bool full = (long)nb * G >= u_lo && (long)(nb + 1) * G <= u_hi;
+    const int col0 = (nb * kColB + wave * kColW) * 16;
+    bool write = true;
+    if (!full) {
+      const int slot = (nb == u_lo / G) ? 0 : 1;
+      float* mine = a.part + (((size_t)v * 2 + slot) * 4 + wave) * kWaveSlotFloats;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < kColW; ++ct) {
+          const int t = mt * kColW + ct;
+          store_agent_f32x4(mine + ((size_t)(t * kSrc) * kWave + lane) * 4, acc[mt][ct]);
+          if (EPI == EPI_SWIGLU)
+            store_agent_f32x4(mine + ((size_t)(t * kSrc + 1) * kWave + lane) * 4, acc[mt][ct + kColW]);
+        }
+      wait_all_memory();
+      __syncthreads();
+      const long U = a.units;
+      const int c_first = (int)((((long)nb * G + 1) * a.nwg - 1) / U);
+      const int c_last = (int)((((long)nb * G + G) * a.nwg - 1) / U);
+      if (tid == 0) s_ticket = take_ticket(&a.counters[nb]);
+      __syncthreads();
+      write = s_ticket == (uint32_t)(c_last - c_first);
+      if (write) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int ct = 0; ct < kColW; ++ct) {
+            const int t = mt * kColW + ct;
+            f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+            for (int c = c_first; c <= c_last; ++c) {
+              const int cslot = (nb == (int)(range_begin(U, c, a.nwg) / G)) ? 0 : 1;
+              const float* src = a.part + (((size_t)c * 2 + cslot) * 4 + wave) * kWaveSlotFloats;
+              sa += load_agent_f32x4(src + ((size_t)(t * kSrc) * kWave + lane) * 4);
+              if (EPI == EPI_SWIGLU) sb += load_agent_f32x4(src + ((size_t)(t * kSrc + 1) * kWave + lane) * 4);
+            }
+            acc[mt][ct] = sa;
+            if (EPI == EPI_SWIGLU) acc[mt][ct + kColW] = sb;
+          }
+        if (tid == 0) reset_counter(&a.counters[nb]);
+      }
+    }
+    if (write) {
+      // lane holds rows 4 * kq + r of column lane % 16
+      const int G2 = a.N >> 7;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < kColW; ++ct) {
+          const int ncl = col0 + ct * 16 + ncol;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = mt * 16 + kq * 4 + r;
+            if (m < a.M) {
+              float val;
+              if (EPI == EPI_SWIGLU) {
+                const float gte = acc[mt][ct][r], up = acc[mt][ct + kColW][r];
+                val = gte / (1.0f + __expf(-gte)) * up;
+              } else {
+                val = acc[mt][ct][r];
+                if (a.res) val += h2f(a.res[(size_t)m * a.ldr + ncl]);
+              }
+              const uint16_t h = f2h(val);
+              if (a.y) a.y[(size_t)m * a.ldy + ncl] = h;
+              if (a.yp) store_prepared(a.yp, m, ncl, G2, h);
+            }
+          }
+        }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  // ---- one continuous pipeline over the range's units ----
+  // Step i: issue weights of unit i + 5 and activations of unit i + 2,
+  // write unit i + 1's activations (loaded one step earlier) to the LDS
+  // ring, barrier, let one wave form unit i + 1's row sums, compute unit i,
+  // and flush when unit i ends its N-block's share.
+  // Warm this XCD's L2 with the activations: the workgroups sharing an XCD
+  // (blockIdx % 8) each touch an equal slice, so later activation loads,
+  // issued only one step ahead, hit in L2.
+  {
+    const int per_xcd = a.nwg >= 8 ? a.nwg / 8 : 1;
+    const size_t vecs = (size_t)MT * G * 4 * kWave;  // 16-byte vectors of prepared activations
+    const size_t chunk = (vecs + per_xcd - 1) / per_xcd;
+    const size_t first = (size_t)(b / 8 % per_xcd) * chunk;
+    uint32_t sink = 0;
+    for (size_t e = first + tid; e < first + chunk && e < vecs; e += 256)
+      sink ^= reinterpret_cast<const u32x4*>(a.a)[e][0];
+    if (sink == 0x9E3779B9u && a.M < 0) a.counters[0] = sink;  // keeps the loads
+  }
+  u32x4 ar[MT], ar_next[MT];
+  BStage<MT, NWV> bs[kRingB];
+  load_a(0, ar);
+  store_a(0, ar);
+  load_a(1, ar);
+#pragma unroll
+  for (int j = 0; j < kRingB - 1; ++j) load_b(j, bs[j]);
+  __syncthreads();
+  if (wave == 0) row_sums(0);
+
+#define SS_GEMM_STEP(J)                                                              \
+  {                                                                                  \
+    const int i = i0 + (J);                                                          \
+    if (i >= total) break;                                                           \
+    load_a(i + 2, ar_next);                                                          \
+    load_b(i + kRingB - 1, bs[((J) + kRingB - 1) % kRingB]);                         \
+    store_a(((J) + 1) % kRingA, ar);                                                 \
+    __syncthreads();                                                                 \
+    if (wave == ((i + 1) & 3) && i + 1 < total) row_sums(((J) + 1) % kRingA);        \
+    __builtin_amdgcn_sched_barrier(0);                                               \
+    compute((J) % kRingA, bs[(J) % kRingB]);                                         \
+    _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) ar[mt] = ar_next[mt];          \
+    const int u = u_lo + i;                                                          \
+    if (i == total - 1 || (u + 1) % G == 0) flush(u / G);                            \
+  }
+  for (int i0 = 0; i0 < total; i0 += kRingB) {
+    SS_GEMM_STEP(0)
+    SS_GEMM_STEP(1)
+    SS_GEMM_STEP(2)
+    SS_GEMM_STEP(3)
+    SS_GEMM_STEP(4)
+    SS_GEMM_STEP(5)
+  }
+#undef SS_GEMM_STEP
+}
+
+// ------------------------------------------------------- activation prep
+// x [M][ldx] fp16 -> prepared layout; one thread per (M-tile, group, lane).
+__global__ __launch_bounds__(256) void prepare_activations_kernel(const uint16_t* __restrict__ x, int M,
+                                                                  int ldx, int G, int MT,
+                                                                  uint16_t* __restrict__ out) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= MT * G * kWave) return;
+  const int lane = idx % kWave;
+  const int g = (idx / kWave) % G;
+  const int mt = idx / (kWave * G);
+  const int m = mt * 16 + (lane & 15);
+  const int kq = lane >> 4;
+  uint32_t a[16];
+  if (m < M) {
+    const u32x4* src = reinterpret_cast<const u32x4*>(x + (size_t)m * ldx + g * 128 + kq * 32);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const u32x4 v = src[i];
+      a[4 * i] = v[0];
+      a[4 * i + 1] = v[1];
+      a[4 * i + 2] = v[2];
+      a[4 * i + 3] = v[3];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) a[i] = 0u;
   }
   const _Float16 sixteen = (_Float16)16.0f;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const uint32_t* b = a + 8 * h;
-    u32x4 lo = {pk_lo(b[0], b[2]), pk_lo(b[1], b[3]), pk_lo(b[4], b[6]), pk_lo(b[5], b[7])};
-    u32x4 hi = {pk_hi(b[0], b[2]), pk_hi(b[1], b[3]), pk_hi(b[4], b[6]), pk_hi(b[5], b[7])};
-    frag[h] = bitcast<half8>(lo) * sixteen;
-    frag[2 + h] = bitcast<half8>(hi);
+    const u32x4 lo = {(b[0] & 0xFFFFu) | (b[2] << 16), (b[1] & 0xFFFFu) | (b[3] << 16),
+                      (b[4] & 0xFFFFu) | (b[6] << 16), (b[5] & 0xFFFFu) | (b[7] << 16)};
+    const u32x4 hi = {(b[0] >> 16) | (b[2] & 0xFFFF0000u), (b[1] >> 16) | (b[3] & 0xFFFF0000u),
+                      (b[4] >> 16) | (b[6] & 0xFFFF0000u), (b[5] >> 16) | (b[7] & 0xFFFF0000u)};
+    const half8 lo16 = bitcast<half8>(lo) * sixteen;
+    uint16_t* base = out + (((size_t)mt * G + g) * 4) * kWave * 8;
+    *reinterpret_cast<u32x4*>(base + ((size_t)(h)*kWave + lane) * 8) = bitcast<u32x4>(lo16);
+    *reinterpret_cast<u32x4*>(base + ((size_t)(2 + h) * kWave + lane) * 8) = hi;
   }
 }
 
-// Weight fragments (same slot order) from the lane's 16 packed bytes.
-__device__ __forceinline__ void weight_fragments(const u32x4 w, uint32_t zero, half8 frag[4]) {
-  const uint32_t magic = 0x64006400u;
-  const _Float16 c_lo = (_Float16)(-(1024.0f + (float)zero));
-  const _Float16 c_hi = (_Float16)(-(1024.0f + 16.0f * (float)zero));
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const uint32_t d0 = w[2 * h], d1 = w[2 * h + 1];
-    const uint32_t s0 = d0 >> 8, s1 = d1 >> 8;
-    u32x4 lo = {(d0 & 0x000F000Fu) | magic, (s0 & 0x000F000Fu) | magic, (d1 & 0x000F000Fu) | magic,
-                (s1 & 0x000F000Fu) | magic};
-    u32x4 hi = {(d0 & 0x00F000F0u) | magic, (s0 & 0x00F000F0u) | magic, (d1 & 0x00F000F0u) | magic,
-                (s1 & 0x00F000F0u) | magic};
-    frag[h] = bitcast<half8>(lo) + c_lo;
-    frag[2 + h] = bitcast<half8>(hi) + c_hi;
-  }
+void launch_prepare_activations(const uint16_t* x, int M, int ldx, int K, uint16_t* out, hipStream_t st) {
+  const int G = K / 128, MT = (M + 15) / 16;
+  const int threads = MT * G * kWave;
+  hipLaunchKernelGGL(prepare_activations_kernel, dim3((threads + 255) / 256), dim3(256), 0, st, x, M, ldx, G,
+                     MT, out);
 }
 
-template <int MT, int NW, int EPI>
-struct GemmTile {
-  static constexpr int kTiles = MT * NW;
-};
-
-template <int MT, int NW, int EPI>
-__global__ __launch_bounds__(256) void w4a16_gemm_kernel(
-    W4Ptr w0, W4Ptr w1, int K, int N, const uint16_t* __restrict__ x, int M, int ldx,
-    uint16_t* __restrict__ y, int ldy, const uint16_t* __restrict__ res, int ldr, int nblocks,
-    int nsplit, float* __restrict__ part, uint32_t* __restrict__ counters) {
-  constexpr int kTiles = MT * NW;
-  constexpr int kColTiles = (EPI == EPI_SWIGLU) ? NW / 2 : NW;  // output column tiles per block
-  constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;               // source tiles per output unit
-  constexpr int kChunkOut = 8 / kSrc;                              // output units per LDS chunk
-  static_assert(kTiles >= 1, "empty tile");
-  __shared__ f32x4 red[4][8][kWave];
-  __shared__ uint32_t s_ticket;
-
-  const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
-  const int nb = blockIdx.x % nblocks;
-  const int ks = blockIdx.x / nblocks;
+// ------------------------------------------------------------- prepack
+// Canonical int4 matrix -> kernel-native copy (see W4Ptr).  A pure
+// rearrangement of the same bits; one wave per (tile, group).
+__global__ __launch_bounds__(256) void prepack_w4_kernel(const uint8_t* __restrict__ q,
+                                                         const uint16_t* __restrict__ s,
+                                                         const uint8_t* __restrict__ z, int K, int N,
+                                                         u32x4* __restrict__ qp, uint32_t* __restrict__ szp) {
   const int G = K >> 7;
-  const int g_begin = (int)(((long)ks * G) / nsplit);
-  const int g_end = (int)(((long)(ks + 1) * G) / nsplit);
-  const int ncol = lane & 15;
-  const int kq = lane >> 4;
-  const int col0 = nb * kColTiles * 16;
-
-  // per-tile weight row pointers (row = output column)
-  const uint8_t* qrow[NW];
-  const uint16_t* srow[NW];
-  const uint8_t* zrow[NW];
-#pragma unroll
-  for (int nt = 0; nt < NW; ++nt) {
-    const W4Ptr& w = (EPI == EPI_SWIGLU && nt >= kColTiles) ? w1 : w0;
-    const int col = col0 + (nt % kColTiles) * 16 + ncol;
-    qrow[nt] = w.q + (size_t)col * (K >> 1) + kq * 16;
-    srow[nt] = w.s + (size_t)col * G;
-    zrow[nt] = w.z + (size_t)col * G;
+  const long item = (long)blockIdx.x * 4 + (threadIdx.x >> 6);  // (tile, group)
+  if (item >= (long)(N >> 4) * G) return;
+  const int t = (int)(item / G), g = (int)(item % G);
+  const int lane = lane_id();
+  const int n = t * 16 + (lane & 15), kq = lane >> 4;
+  qp[item * kWave + lane] = *reinterpret_cast<const u32x4*>(q + (size_t)n * (K >> 1) + (size_t)g * 64 + kq * 16);
+  if (lane < 16) {
+    const size_t si = (size_t)n * G + g;
+    szp[item * 16 + lane] = (uint32_t)s[si] | ((uint32_t)z[si] << 16);
   }
-  const uint16_t* xrow[MT];
-  bool xvalid[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = mt * 16 + ncol;
-    xvalid[mt] = m < M;
-    xrow[mt] = x + (size_t)(xvalid[mt] ? m : 0) * ldx + kq * 32;
-  }
+}
 
-  f32x4 acc[MT][NW];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < NW; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  u32x4 a_cur[MT][4], b_cur[NW];
-  uint16_t s_cur[NW];
-  uint8_t z_cur[NW];
-  auto load_group = [&](int g, u32x4 (&a_raw)[MT][4], u32x4 (&b_raw)[NW], uint16_t (&s_raw)[NW],
-                        uint8_t (&z_raw)[NW]) {
-#pragma unroll
-    for (int nt = 0; nt < NW; ++nt) {
-      b_raw[nt] = *reinterpret_cast<const u32x4*>(qrow[nt] + (size_t)g * 64);
-      s_raw[nt] = srow[nt][g];
-      z_raw[nt] = zrow[nt][g];
-    }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const u32x4* src = reinterpret_cast<const u32x4*>(xrow[mt] + (size_t)g * 128);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a_raw[mt][i] = xvalid[mt] ? src[i] : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-
-  int g = g_begin + wave;
-  if (g < g_end) load_group(g, a_cur, b_cur, s_cur, z_cur);
-  for (; g < g_end; g += 4) {
-    u32x4 a_nxt[MT][4], b_nxt[NW];
-    uint16_t s_nxt[NW];
-    uint8_t z_nxt[NW];
-    const bool more = g + 4 < g_end;
-    if (more) load_group(g + 4, a_nxt, b_nxt, s_nxt, z_nxt);
-
-    half8 afrag[MT][4];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) act_fragments(a_cur[mt], afrag[mt]);
-#pragma unroll
-    for (int nt = 0; nt < NW; ++nt) {
-      half8 bfrag[4];
-      weight_fragments(b_cur[nt], z_cur[nt], bfrag);
-      const float sc = h2f(s_cur[nt]) * 0.0625f;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 c = {0.f, 0.f, 0.f, 0.f};
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(afrag[mt][0], bfrag[0], c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(afrag[mt][1], bfrag[1], c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(afrag[mt][2], bfrag[2], c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(afrag[mt][3], bfrag[3], c, 0, 0, 0);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[mt][nt][r] = __builtin_fmaf(c[r], sc, acc[mt][nt][r]);
-      }
-    }
-    if (more) {
-#pragma unroll
-      for (int nt = 0; nt < NW; ++nt) {
-        b_cur[nt] = b_nxt[nt];
-        s_cur[nt] = s_nxt[nt];
-        z_cur[nt] = z_nxt[nt];
-      }
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) a_cur[mt][i] = a_nxt[mt][i];
-    }
-  }
-
-  // ---- reduce the 4 waves' K-slices through LDS (fixed order) ----
-  // Output unit u (a column tile, or a (gate, up) tile pair for SwiGLU):
-  // mt = u / kColTiles, ct = u % kColTiles; wave w finishes units u = w + 4 j.
-  // Units go through LDS in chunks of at most 8 source tiles (32 KB).
-  constexpr int kOut = MT * kColTiles;
-  constexpr int kJ = (kOut + 3) / 4;
-  f32x4 sum_a[kJ], sum_b[kJ];
-#pragma unroll
-  for (int u0 = 0; u0 < kOut; u0 += kChunkOut) {
-#pragma unroll
-    for (int du = 0; du < kChunkOut; ++du) {
-      const int u = u0 + du;
-      if (u < kOut) {
-        const int mt = u / kColTiles, ct = u % kColTiles;
-        red[wave][du * kSrc][lane] = acc[mt][ct];
-        if (EPI == EPI_SWIGLU) red[wave][du * kSrc + 1][lane] = acc[mt][ct + kColTiles];
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kChunkOut / 4; ++j) {
-      const int du = wave + 4 * j;
-      const int J = u0 / 4 + j;
-      if (J < kJ && u0 + du < kOut) {
-        const int ta = du * kSrc;
-        sum_a[J] = red[0][ta][lane] + red[1][ta][lane] + red[2][ta][lane] + red[3][ta][lane];
-        if (EPI == EPI_SWIGLU)
-          sum_b[J] = red[0][ta + 1][lane] + red[1][ta + 1][lane] + red[2][ta + 1][lane] + red[3][ta + 1][lane];
-      }
-    }
-    __syncthreads();
-  }
-
-  if (nsplit > 1) {
-    // publish this split's partial, then the last arriving split combines
-    constexpr int kParts = kSrc;
-    float* mine = part + ((size_t)(nb * nsplit + ks) * kOut * kParts) * kWave * 4;
-#pragma unroll
-    for (int j = 0; j < kJ; ++j) {
-      const int t = wave + 4 * j;
-      if (t < kOut) {
-        store_agent_f32x4(mine + ((size_t)(t * kParts) * kWave + lane) * 4, sum_a[j]);
-        if (EPI == EPI_SWIGLU) store_agent_f32x4(mine + ((size_t)(t * kParts + 1) * kWave + lane) * 4, sum_b[j]);
-      }
-    }
-    wait_all_memory();
-    __syncthreads();
-    if (threadIdx.x == 0) s_ticket = take_ticket(&counters[nb]);
-    __syncthreads();
-    if (s_ticket != (uint32_t)(nsplit - 1)) return;
-#pragma unroll
-    for (int j = 0; j < kJ; ++j) {
-      const int t = wave + 4 * j;
-      if (t < kOut) {
-        f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < nsplit; ++s) {
-          const float* src = part + ((size_t)(nb * nsplit + s) * kOut * kParts) * kWave * 4;
-          sa += load_agent_f32x4(src + ((size_t)(t * kParts) * kWave + lane) * 4);
-          if (EPI == EPI_SWIGLU) sb += load_agent_f32x4(src + ((size_t)(t * kParts + 1) * kWave + lane) * 4);
-        }
-        sum_a[j] = sa;
-        sum_b[j] = sb;
-      }
-    }
-    if (threadIdx.x == 0) reset_counter(&counters[nb]);
-  }
-
-  // ---- epilogue: lane holds rows 4 * (lane / 16) + r of column lane % 16 ----
-#pragma unroll
-  for (int j = 0; j < kJ; ++j) {
-    const int t = wave + 4 * j;
-    if (t < kOut) {
-      const int mt = t / kColTiles, ct = t % kColTiles;
-      const int n = col0 + ct * 16 + ncol;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = mt * 16 + kq * 4 + r;
-        if (m < M) {
-          float v;
-          if (EPI == EPI_SWIGLU) {
-            const float gte = sum_a[j][r], up = sum_b[j][r];
-            v = gte / (1.0f + __expf(-gte)) * up;
-          } else {
-            v = sum_a[j][r];
-            if (res) v += h2f(res[(size_t)m * ldr + n]);
-          }
-          y[(size_t)m * ldy + n] = f2h(v);
-        }
-      }
-    }
-  }
+void launch_prepack_w4(const uint8_t* q, const uint16_t* s, const uint8_t* z, int K, int N, void* packed,
+                       hipStream_t st) {
+  const long items = (long)(N / 16) * (K / 128);
+  u32x4* qp = reinterpret_cast<u32x4*>(packed);
+  uint32_t* szp = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(packed) + (size_t)K * N / 2);
+  hipLaunchKernelGGL(prepack_w4_kernel, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, q, s, z, K, N, qp,
+                     szp);
 }
 
 // ----------------------------------------------------------------- launch
 
 template <int MT, int NW, int EPI>
 static void launch_t(const GemmLaunch& L, hipStream_t st) {
-  W4Ptr a{L.w0.q, L.w0.s, L.w0.z}, b{L.w1.q, L.w1.s, L.w1.z};
-  hipLaunchKernelGGL((w4a16_gemm_kernel<MT, NW, EPI>), dim3(L.nblocks * L.nsplit), dim3(256), 0, st,
-                     a, b, L.K, L.N, L.x, L.M, L.ldx, L.y, L.ldy, L.res, L.ldr, L.nblocks, L.nsplit,
-                     L.part, L.counters);
+  GemmArgs a;
+  auto unpack = [&](const void* p) {
+    return W4Ptr{reinterpret_cast<const u32x4*>(p),
+                 reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(p) + (size_t)L.K * L.N / 2)};
+  };
+  a.w0 = unpack(L.w0);
+  a.w1 = unpack(L.w1);
+  a.K = L.K;
+  a.N = L.N;
+  a.G = L.K / 128;
+  a.a = L.aprep;
+  a.M = L.M;
+  a.y = L.y;
+  a.ldy = L.ldy;
+  a.yp = L.yprep;
+  a.res = L.res;
+  a.ldr = L.ldr;
+  a.nblocks = L.nblocks;
+  a.nwg = L.nwg;
+  a.units = (long)L.nblocks * a.G;
+  a.part = L.part;
+  a.counters = L.counters;
+  hipLaunchKernelGGL((w4a16_gemm_kernel<MT, NW, EPI>), dim3(L.nwg), dim3(256), 0, st, a);
 }
 
 template <int MT, int EPI>
@@ -334,34 +455,25 @@ void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st) {
   else launch_mt<EPI_PLAIN>(L, st);
 }
 
-}  // namespace ss
-
-namespace ss {
-
 GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
+  // nw = 16-column source tiles per wave (SwiGLU: half gate, half up); a
+  // block (one workgroup's N-range) holds 4 waves' tiles
   GemmPlan p;
   const int tiles = N / 16;
   const int MT = (M + 15) / 16;
   if (swiglu) {
-    p.nw = (tiles % 2 == 0) ? 4 : 2;
-    p.nblocks = tiles / (p.nw / 2);
+    p.nw = 2;  // one gate and one up tile per wave
+    p.nblocks = tiles / 4;
   } else {
-    p.nw = (tiles % 4 == 0) ? 4 : (tiles % 2 == 0 ? 2 : 1);
-    p.nblocks = tiles / p.nw;
+    p.nw = (MT <= 2 && tiles % 8 == 0) ? 2 : 1;
+    p.nblocks = tiles / (4 * p.nw);
   }
-  // about two workgroups per CU; every wave keeps at least one group per split
-  const int G = K / 128;
-  const int target = 512;
-  int ns = (target + p.nblocks - 1) / p.nblocks;
-  int max_split = G / 4;
-  if (max_split < 1) max_split = 1;
-  if (ns > max_split) ns = max_split;
-  if (ns > 32) ns = 32;
-  if (ns < 1) ns = 1;
-  p.nsplit = ns;
-  const int col_tiles = swiglu ? p.nw / 2 : p.nw;
+  const long units = (long)p.nblocks * (K / 128);
+  p.nwg = (int)(units < kGemmWorkgroups ? units : kGemmWorkgroups);
+  const int col_w = swiglu ? p.nw / 2 : p.nw;
   const int src = swiglu ? 2 : 1;
-  p.part_bytes = ns > 1 ? (size_t)p.nblocks * ns * MT * col_tiles * src * kWave * 16 : 0;
+  p.part_bytes = (size_t)p.nwg * 2 * 4 * MT * col_w * src * kWave * 16;
+  p.prep_bytes = (size_t)MT * (K / 128) * 4 * kWave * 16;
   return p;
 }
 

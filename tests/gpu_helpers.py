@@ -45,8 +45,11 @@ def check_close(got_bits, ref_bits, what=""):
 
 
 def upload_w4(W):
+    """Upload a canonical int4 matrix and build its kernel-native copy."""
     t = (up(W["qweight"]), up(W["scales"]), up(W["zeros"]))
-    return t, ss.make_w4(*t)
+    d = ss.make_w4(*t)
+    packed = ss.prepack_w4(d)
+    return t + (packed,), d
 
 
 class DeviceLayer:

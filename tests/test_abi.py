@@ -46,12 +46,16 @@ def test_status_strings(ss):
 def test_host_side_validation_rejects_before_launch(ss):
     lib = ss.lib()
     fake = 0x10000  # never dereferenced: validation fails first
-    W = ss.W4(fake, fake, fake, 4096, 1024)
+    W = ss.W4(fake, fake, fake, 4096, 1024, fake)
     ws_small = 16
     # null weight descriptor
     assert lib.swiftspec_w4a16_gemm(None, fake, 8, 4096, fake, 1024, None, 0, fake, 1 << 30, None) == ss.INVALID_ARG
     # K not a multiple of the quantisation group
-    W_bad = ss.W4(fake, fake, fake, 4000, 1024)
+    W_bad = ss.W4(fake, fake, fake, 4000, 1024, fake)
+    W_unpacked = ss.W4(fake, fake, fake, 4096, 1024, None)
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W_unpacked), fake, 8, 4096, fake, 1024, None, 0, fake, 1 << 30,
+                                    None) == ss.INVALID_ARG
+    assert lib.swiftspec_w4_packed_bytes(4096, 1024) == 4096 * 1024 // 2 + 1024 * 32 * 4
     assert lib.swiftspec_w4a16_gemm(ctypes.byref(W_bad), fake, 8, 4096, fake, 1024, None, 0, fake, 1 << 30,
                                     None) == ss.UNSUPPORTED
     # too many rows

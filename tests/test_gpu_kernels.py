@@ -191,7 +191,7 @@ def _gemm_case(M, K, N, seed, residual):
 
 @pytest.mark.parametrize("M", [1, 8, 13, 16, 32, 40, 64])
 def test_w4a16_gemm_small_shapes_ragged_M(M):
-    _gemm_case(M, 1024, 272, seed=M, residual=(M % 2 == 0))
+    _gemm_case(M, 1024, 320, seed=M, residual=(M % 2 == 0))
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
@@ -354,3 +354,66 @@ def test_tree_attention_invalid_tree_or_prefix_sets_error_and_writes_nothing():
                           up(np.array([P], np.int32)), up(parent), s.Hq, s.Hkv, s.D, rope, out, ws)
         assert ss.read_device_error(ws) & bit
         assert torch.all(out == 7) and torch.all(kc == 0) and torch.all(vc == 0)
+
+
+# ------------------------------------------------------- layouts (bit-exact)
+
+
+def test_prepack_is_a_bit_exact_rearrangement():
+    K, N = 512, 192
+    W = _rand_w4(31, N, K)
+    t, d = upload_w4(W)
+    packed = t[3].cpu().numpy()
+    G = K // 128
+    qp = packed[:K * N // 2].reshape(N // 16, G, 64, 16)
+    szp = packed[K * N // 2:].view(np.uint32).reshape(N // 16, G, 16)
+    q, s_, z = W["qweight"], W["scales"], W["zeros"]
+    for tile in range(N // 16):
+        for g in range(G):
+            for lane in range(64):
+                n, kq = tile * 16 + lane % 16, lane // 16
+                assert np.array_equal(qp[tile, g, lane], q[n, g * 64 + kq * 16:g * 64 + kq * 16 + 16])
+            for c in range(16):
+                n = tile * 16 + c
+                assert szp[tile, g, c] == int(s_[n, g]) | (int(z[n, g]) << 16)
+
+
+def test_prepared_activation_layout_is_bit_exact():
+    M, K = 21, 256
+    x = gen.normal_f16(32, 0, (M, K))
+    xp = torch.zeros(ss.prepared_bytes(M, K), dtype=torch.uint8, device=dev())
+    ss.prepare_activations(up(x), xp)
+    torch.cuda.synchronize()
+    got = xp.cpu().numpy().view(np.uint16)
+    G = K // 128
+    exp = np.zeros(((M + 15) // 16, G, 4, 64, 8), np.uint16)
+    order = [0, 4, 2, 6, 8, 12, 10, 14]
+    xf = x.view(np.float16)
+    for m in range(M):
+        for k0 in range(0, K, 32):
+            g, kq = k0 // 128, (k0 % 128) // 32
+            lane = kq * 16 + m % 16
+            for f in range(4):
+                base = k0 + 16 * (f % 2) + (f // 2)  # even k for f < 2, odd k for f >= 2
+                vals = np.array([xf[m, base + o] for o in order], np.float16)
+                if f < 2:
+                    vals = (vals.astype(np.float32) * 16).astype(np.float16)
+                exp[m // 16, g, f, lane] = vals.view(np.uint16)
+    assert np.array_equal(got.reshape(exp.shape), exp)
+
+
+def test_prepared_gemm_entry_matches_plain_entry_bitwise():
+    M, K, N = 24, 1024, 256
+    W = _rand_w4(33, N, K)
+    t, d = upload_w4(W)
+    x = gen.normal_f16(34, 0, (M, K))
+    dx = up(x)
+    y1 = torch.zeros((M, N), dtype=torch.int16, device=dev())
+    y2 = torch.zeros_like(y1)
+    ws = ss.workspace(ss.gemm_workspace_bytes(M, K, N), dev())
+    ss.w4a16_gemm(d, dx, y1, ws)
+    xp = torch.zeros(ss.prepared_bytes(M, K), dtype=torch.uint8, device=dev())
+    ss.prepare_activations(dx, xp)
+    ss.w4a16_gemm_prepared(d, xp, M, y2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)

@@ -26,8 +26,7 @@ struct GemmLaunch {
   int nblocks;  // column blocks
   int nwg;      // workgroups launched
   bool swiglu;
-  float* part;
-  uint32_t* counters;
+  float* part;  // split-K partial slots (2 per workgroup)
 };
 
 struct GemmPlan {

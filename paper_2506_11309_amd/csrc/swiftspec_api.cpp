@@ -56,10 +56,6 @@ int check_w4(const swiftspec_w4* W) {
 
 constexpr int kMaxCounters = (int)((SWIFTSPEC_WS_HEADER_BYTES - 256u) / 4u);
 
-bool gemm_counters_fit(int M, int K, int N, bool swiglu) {
-  return ss::plan_w4a16_gemm(M, K, N, swiglu).nblocks <= kMaxCounters;
-}
-
 bool attn_counters_fit(int T, int Hq, int Hkv) {
   const long R = (long)T * (Hq / Hkv);
   return (long)Hkv * ((R + 63) / 64) <= kMaxCounters;
@@ -93,7 +89,6 @@ void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* ap
   L.nwg = p.nwg;
   L.swiglu = swiglu;
   L.part = part;
-  L.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + 256);
   ss::launch_w4a16_gemm(L, st);
 }
 
@@ -269,7 +264,6 @@ int swiftspec_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, in
   if (!aligned16(x) || ldx % 8) return SWIFTSPEC_MISALIGNED;
   if (residual == y && ldr != ldy) return SWIFTSPEC_INVALID_ARG;
   if (M == 0) return SWIFTSPEC_OK;
-  if (!gemm_counters_fit(M, W->K, W->N, false)) return SWIFTSPEC_UNSUPPORTED;
   if (ws_bytes < gemm_ws(M, W->K, W->N, false)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   run_gemm_plain(W, nullptr, x, M, ldx, y, ldy, residual, ldr, ws, S(stream));
   return check_launch();
@@ -288,7 +282,6 @@ int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const
   if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
   if (!aligned16(x) || ldx % 8) return SWIFTSPEC_MISALIGNED;
   if (M == 0) return SWIFTSPEC_OK;
-  if (!gemm_counters_fit(M, Wg->K, Wg->N, true)) return SWIFTSPEC_UNSUPPORTED;
   if (ws_bytes < gemm_ws(M, Wg->K, Wg->N, true)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   run_gemm_plain(Wg, Wu, x, M, ldx, y, ldy, nullptr, 0, ws, S(stream));
   return check_launch();
@@ -319,7 +312,6 @@ int swiftspec_w4a16_gemm_prepared(const swiftspec_w4* W, const uint16_t* xp, int
   if (!aligned16(xp)) return SWIFTSPEC_MISALIGNED;
   if (residual == y && ldr != ldy) return SWIFTSPEC_INVALID_ARG;
   if (M == 0) return SWIFTSPEC_OK;
-  if (!gemm_counters_fit(M, W->K, W->N, false)) return SWIFTSPEC_UNSUPPORTED;
   ss::GemmPlan p = ss::plan_w4a16_gemm(M, W->K, W->N, false);
   if (ws_bytes < kHeader + align_up(p.part_bytes)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   run_gemm(W, nullptr, xp, M, y, ldy, nullptr, residual, ldr, ws,
@@ -339,7 +331,6 @@ int swiftspec_w4a16_swiglu_prepared(const swiftspec_w4* Wg, const swiftspec_w4* 
   if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
   if (!aligned16(xp)) return SWIFTSPEC_MISALIGNED;
   if (M == 0) return SWIFTSPEC_OK;
-  if (!gemm_counters_fit(M, Wg->K, Wg->N, true)) return SWIFTSPEC_UNSUPPORTED;
   ss::GemmPlan p = ss::plan_w4a16_gemm(M, Wg->K, Wg->N, true);
   if (ws_bytes < kHeader + align_up(p.part_bytes)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   run_gemm(Wg, Wu, xp, M, y, ldy, nullptr, nullptr, 0, ws,
@@ -458,9 +449,7 @@ int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, u
   if (T < 1 || d->H < 1 || d->Hq < 1 || d->Hkv < 1 || d->F < 1 || d->S_max < T) return SWIFTSPEC_INVALID_ARG;
   if (T > SWIFTSPEC_MAX_TREE || (d->D != 64 && d->D != 128) || d->Hq % d->Hkv) return SWIFTSPEC_UNSUPPORTED;
   const int H = d->H, Hd = d->Hq * d->D, Nqkv = (d->Hq + 2 * d->Hkv) * d->D, F = d->F;
-  if (!attn_counters_fit(T, d->Hq, d->Hkv) || !gemm_counters_fit(T, F, H, false) ||
-      !gemm_counters_fit(T, H, F, true) || !gemm_counters_fit(T, H, Nqkv, false))
-    return SWIFTSPEC_UNSUPPORTED;
+  if (!attn_counters_fit(T, d->Hq, d->Hkv)) return SWIFTSPEC_UNSUPPORTED;
   int rc;
   if ((rc = check_w4(&Lw->wqkv)) || (rc = check_w4(&Lw->wo)) || (rc = check_w4(&Lw->wgate)) ||
       (rc = check_w4(&Lw->wup)) || (rc = check_w4(&Lw->wdown)))

@@ -11,16 +11,22 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
                                                       const uint16_t* __restrict__ gamma, float eps,
                                                       uint16_t* __restrict__ out, int ldo,
                                                       uint16_t* __restrict__ out_prep) {
+  // one workgroup per row; thread t owns the 32-element chunks c = t + 256 i
+  // (k = 32 c .. 32 c + 31), i.e. one prepared fragment set each
   __shared__ float partial[4];
   const int m = blockIdx.x;
   const uint16_t* xr = x + (size_t)m * ldx;
+  const int nch = H >> 5;
   float ss = 0.f;
-  for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
-    half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + c));
+  for (int c = threadIdx.x; c < nch; c += 256) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float v = (float)h[e];
-      ss = __builtin_fmaf(v, v, ss);
+    for (int q = 0; q < 4; ++q) {
+      half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = (float)h[e];
+        ss = __builtin_fmaf(v, v, ss);
+      }
     }
   }
 #pragma unroll
@@ -30,18 +36,28 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
   const float total = (partial[0] + partial[1]) + (partial[2] + partial[3]);
   const float inv = 1.0f / sqrtf(total / (float)H + eps);
   uint16_t* orow = out + (size_t)m * ldo;
-  for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
-    half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + c));
-    half8 gm = bitcast<half8>(*reinterpret_cast<const u32x4*>(gamma + c));
-    half8 o;
+  const int G = H >> 7;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    uint32_t w[16];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (_Float16)(((float)h[e] * inv) * (float)gm[e]);
-    *reinterpret_cast<u32x4*>(orow + c) = bitcast<u32x4>(o);
-    if (out_prep) {
+    for (int q = 0; q < 4; ++q) {
+      const half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q));
+      const half8 gm = bitcast<half8>(*reinterpret_cast<const u32x4*>(gamma + 32 * c + 8 * q));
+      half8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (_Float16)(((float)h[e] * inv) * (float)gm[e]);
       const u32x4 ob = bitcast<u32x4>(o);
+      *reinterpret_cast<u32x4*>(orow + 32 * c + 8 * q) = ob;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        store_prepared(out_prep, m, c + e, H >> 7, (uint16_t)(ob[e >> 1] >> (16 * (e & 1))));
+      for (int e = 0; e < 4; ++e) w[4 * q + e] = ob[e];
+    }
+    if (out_prep) {
+      u32x4 f[4];
+      pack_prepared(w, f);
+      const int g = c >> 2, kq = c & 3;
+      uint16_t* base = out_prep + ((((size_t)(m >> 4) * G + g) * 4) * kWave + kq * 16 + (m & 15)) * 8;
+#pragma unroll
+      for (int fi = 0; fi < 4; ++fi) *reinterpret_cast<u32x4*>(base + (size_t)fi * kWave * 8) = f[fi];
     }
   }
 }

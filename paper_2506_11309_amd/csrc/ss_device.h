@@ -113,6 +113,16 @@ __device__ __forceinline__ f32x4 load_agent_f32x4(const float* p) {
   return f32x4{a[0], a[1], b[0], b[1]};
 }
 
+// Workgroup barrier without a memory fence: s_barrier after the wave's own
+// LDS traffic has completed.  __syncthreads() would also wait for every
+// outstanding global load (prefetched tiles); the empty asm statements
+// with a memory clobber keep the compiler from moving LDS accesses across.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Wait until every outstanding memory operation of this wave has completed
 // (stores acknowledged at their coherence scope).
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
@@ -159,6 +169,26 @@ __device__ __forceinline__ void store_prepared(uint16_t* prep, int m, int k, int
     __builtin_memcpy(&h, &v, 2);
   }
   prep[off] = h;
+}
+
+// Prepared-layout fragments of 32 consecutive activations k = 128 g + 32 kq
+// + t, t = 0..31, of one row, given as 16 u32 (element t in half t % 2 of
+// word t / 2): fragment 0 holds even t < 16, 1 even t >= 16 (both x 16), 2
+// odd t < 16, 3 odd t >= 16, each in slot order u = 0, 2, 1, 3, 4, 6, 5, 7
+// of u = (t % 16) / 2 -- the order prep_offset describes.  They belong at
+// ((((m / 16) * G + g) * 4 + f) * 64 + kq * 16 + m % 16) * 8 halves.
+__device__ __forceinline__ void pack_prepared(const uint32_t (&a)[16], u32x4 (&f)[4]) {
+  const _Float16 sixteen = (_Float16)16.0f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t* b = a + 8 * h;
+    const u32x4 lo = {(b[0] & 0xFFFFu) | (b[2] << 16), (b[1] & 0xFFFFu) | (b[3] << 16),
+                      (b[4] & 0xFFFFu) | (b[6] << 16), (b[5] & 0xFFFFu) | (b[7] << 16)};
+    const u32x4 hi = {(b[0] >> 16) | (b[2] & 0xFFFF0000u), (b[1] >> 16) | (b[3] & 0xFFFF0000u),
+                      (b[4] >> 16) | (b[6] & 0xFFFF0000u), (b[5] >> 16) | (b[7] & 0xFFFF0000u)};
+    f[h] = bitcast<u32x4>(bitcast<half8>(lo) * sixteen);
+    f[2 + h] = hi;
+  }
 }
 
 }  // namespace ss

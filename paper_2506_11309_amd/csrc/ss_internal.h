@@ -8,9 +8,6 @@
 
 namespace ss {
 
-// Fixed grid of the stream-K GEMMs: two 4-wave workgroups per CU of MI355X.
-constexpr int kGemmWorkgroups = 512;
-
 struct GemmLaunch {
   const void* w0;  // kernel-native (prepacked) weights
   const void* w1;  // up-projection of the fused SwiGLU

@@ -3,29 +3,37 @@
 // square mask; Sec. 3.3 masked attention; Sec. 4 positions from tree depth).
 //
 // Query rows of one kv head g: r = i * G + hh (node i, query head g*G + hh),
-// R = T * G rows.  Workgroup = 4 waves = 64 query rows (one 16-row tile per
-// wave).  Grid = Hkv x RB x (S + 1):
+// R = T * G rows.  Workgroup = W waves = 16 W query rows (one 16-row tile
+// per wave), W = 8 for R >= 128, else 4.  Grid = Hkv x RB x (S + 1):
 //   * splits 0..S-1 each take a contiguous chunk of the prefix keys [0, P)
 //     (P is read on the device, so one launch shape serves every step);
 //   * split S takes the T tree keys: it rotates the tree's keys, applies the
 //     ancestor mask, and (row block 0 only) writes rotated keys and values
 //     to cache rows [P, P+T).  Tree keys are consumed from registers/LDS, so
 //     no workgroup reads a cache row another one is writing.
+// Prefix keys stream in 64-key tiles: each thread loads its share of a
+// tile's K and V rows into a 5-deep register ring (tiles t+1..t+4 in
+// flight while tile t is computed), writes them row-major to a 3-slot LDS
+// ring, and a fence-free barrier per tile hands the tile to all waves.
 // Scores use S^T = K . Q^T on v_mfma_f32_16x16x32_f16: the result leaves
 // each lane with four consecutive keys of one query row, which is exactly
 // the A-operand layout the P.V product needs (keys are the reduction index),
-// so probabilities never leave registers.  V is staged transposed in LDS so
-// its B fragments are two 8-byte LDS reads.  Online softmax in fp32.
+// so probabilities never leave registers.  The V B-operand (key-major per d
+// column) comes from the row-major tile through ds_read_b64_tr_b16: in each
+// 16-lane group, lane j receives element j % 4 of the 8-byte rows addressed
+// by lanes j / 4 + 4e, e = 0..3.  Online softmax in fp32, base 2.
 // The S + 1 partial results (unnormalised O, running max, running sum) of a
-// row block are merged by the last workgroup to arrive (atomic ticket), in
-// split order, so results are deterministic.  blockIdx % Hkv = g keeps one
-// head's workgroups on one XCD when Hkv divides 8.
+// row block are merged by a second kernel on the same stream, in split
+// order, so results are deterministic.  blockIdx % Hkv = g keeps one head's
+// workgroups on one XCD when Hkv divides 8.
 #include "ss_device.h"
 #include "ss_internal.h"
 
 namespace ss {
 
 constexpr int kKeyTile = 64;
+constexpr int kAttnRing = 5;  // register ring of K/V tiles
+constexpr int kAttnLds = 3;   // LDS ring of K/V tiles
 
 struct AttnArgs {
   const uint16_t* q;
@@ -44,29 +52,36 @@ struct AttnArgs {
   float scale_log2;  // softmax scale * log2(e)
 };
 
-template <int D>
-struct AttnSmem {
-  static constexpr int kKStride = D + 8;         // halves per K row (pad: 16 B)
-  static constexpr int kVStride = kKeyTile + 4;  // halves per V^T row (pad: 8 B)
-  uint16_t k[kKeyTile * kKStride];
-  uint16_t vt[D * kVStride];
-  uint64_t anc[64];
-  int32_t depth[64];
-  int32_t status;
-  uint32_t ticket;
-};
+typedef short v4i16 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ float exp2_approx(float x) { return exp2f(x); }
-
+// Bytes of one workgroup's partial: O normalised by its row sum, fp16
+// [W waves][D/16 d-tiles][64 lanes][4 rows], then fp32 (max, sum) of its
+// 16 W rows.  Normalised values are bounded by max |v|, so fp16 holds them
+// with the output's own precision.
 template <int D>
-__global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
-  constexpr int KS = D / 32;  // k-steps of the QK^T product
-  constexpr int DT = D / 16;  // d tiles of the PV product
+__host__ __device__ constexpr size_t attn_part_bytes(int waves) {
+  return (size_t)waves * (D / 16) * kWave * 8 + (size_t)waves * 16 * 8;
+}
+
+template <int D, int W>
+__global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
+  constexpr int NT = 64 * W;         // threads
+  constexpr int KS = D / 32;         // k-steps of the QK^T product
+  constexpr int DT = D / 16;         // d tiles of the PV product
   constexpr int HALF = D / 2;
-  __shared__ AttnSmem<D> sm;
+  constexpr int KST = D + 16;        // halves per LDS row (32-byte pad)
+  constexpr int VPR = D / 8;         // 16-byte vectors per key row
+  constexpr int NV = kKeyTile * VPR / NT;  // vectors per thread per matrix per tile
+  static_assert(NV >= 1 && kKeyTile * VPR % NT == 0, "tile split");
+  __shared__ uint16_t ks[kAttnLds][kKeyTile * KST];
+  __shared__ uint16_t vs[kAttnLds][kKeyTile * KST];
+  __shared__ uint64_t s_anc[64];
+  __shared__ int32_t s_depth[64];
+  __shared__ int32_t s_status;
 
+  const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n16 = lane & 15;
   const int kq = lane >> 4;
   const int g = blockIdx.x % a.Hkv;
@@ -80,25 +95,31 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
     uint64_t anc;
     int depth;
     const bool ok = tree_masks_wave(a.parent, a.T, anc, depth);
-    if (lane < 64) {
-      sm.anc[lane] = anc;
-      sm.depth[lane] = depth;
-    }
+    s_anc[lane] = anc;
+    s_depth[lane] = depth;
     if (lane == 0) {
       const int P = *a.prefix_len;
       int st = 0;
       if (!ok) st |= SWIFTSPEC_DEVERR_BAD_TREE;
       if (P < 0 || P > a.S_max - a.T) st |= SWIFTSPEC_DEVERR_BAD_PREFIX;
-      sm.status = st;
+      s_status = st;
       if (st && blockIdx.x == 0) report_error(a.ws, (uint32_t)st);
     }
   }
   __syncthreads();
-  if (sm.status) return;
+  const int nparts = a.nsplit + 1;
+  const size_t grp = (size_t)g * a.RB + rb;
+  char* mine = reinterpret_cast<char*>(a.part) + (grp * nparts + sp) * attn_part_bytes<D>(W);
+  float* ml = reinterpret_cast<float*>(mine + (size_t)W * (D / 16) * kWave * 8);
+  if (s_status) {
+    // invalid tree or prefix: empty partials, so the merge leaves the output alone
+    if (tid < 16 * W) *reinterpret_cast<f32x2*>(ml + tid * 2) = f32x2{-INFINITY, 0.f};
+    return;
+  }
   const int P = *a.prefix_len;
 
   // ---- this wave's 16 query rows: rotated Q as B fragments ----
-  const int row = rb * 64 + wave * 16 + n16;
+  const int row = rb * (16 * W) + wave * 16 + n16;
   const bool row_ok = row < a.R;
   const int node = row_ok ? row / a.G : 0;
   const int qhead = g * a.G + (row_ok ? row % a.G : 0);
@@ -113,16 +134,16 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) qv[j][e] = (float)h[e];
     }
-    const float* cs = a.rope + (size_t)(P + sm.depth[node]) * D;  // [D/2][2]
+    const float* cs = a.rope + (size_t)(P + s_depth[node]) * D;  // [D/2][2]
 #pragma unroll
     for (int j = 0; j < KS / 2; ++j) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int d = 32 * j + 8 * kq + e;  // < D/2; partner d + D/2 sits in k-step j + KS/2
-        const float c = cs[2 * d], s = cs[2 * d + 1];
+        const float c = cs[2 * d], sn = cs[2 * d + 1];
         const float x1 = qv[j][e], x2 = qv[j + KS / 2][e];
-        qv[j][e] = x1 * c - x2 * s;
-        qv[j + KS / 2][e] = x2 * c + x1 * s;
+        qv[j][e] = x1 * c - x2 * sn;
+        qv[j + KS / 2][e] = x2 * c + x1 * sn;
       }
     }
 #pragma unroll
@@ -134,98 +155,19 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
     }
   }
 
-  // ---- key range ----
-  int k_lo = 0, k_hi = 0;
-  if (!tree_split) {
-    const int per = (P + a.nsplit - 1) / a.nsplit;
-    const int chunk = ((per + kKeyTile - 1) / kKeyTile) * kKeyTile;
-    k_lo = min(P, sp * chunk);
-    k_hi = min(P, k_lo + chunk);
-  }
-
   float m_run = -INFINITY, l_run = 0.f;  // for row n16 of this wave (replicated over kq)
   f32x4 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const uint64_t anc = s_anc[node];
 
-  const uint16_t* kc = a.k_cache + (size_t)g * a.S_max * D;
-  const uint16_t* vc = a.v_cache + (size_t)g * a.S_max * D;
-  constexpr int kVecPerRow = D / 8;                       // 16-byte vectors per key row
-  constexpr int kVecPerThread = kKeyTile * kVecPerRow / 256;  // per tile, for K and for V
-
-  const int ntiles = tree_split ? 1 : (k_hi - k_lo + kKeyTile - 1) / kKeyTile;
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int key0 = k_lo + tile * kKeyTile;
-    // ---- stage K (row-major) and V (transposed) into LDS ----
-    if (!tree_split) {
-#pragma unroll
-      for (int it = 0; it < kVecPerThread; ++it) {
-        const int idx = threadIdx.x + it * 256;
-        const int kr = idx / kVecPerRow, c8 = (idx % kVecPerRow) * 8;
-        const int key = key0 + kr;
-        u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-        if (key < k_hi) {
-          kv = *reinterpret_cast<const u32x4*>(kc + (size_t)key * D + c8);
-          vv = *reinterpret_cast<const u32x4*>(vc + (size_t)key * D + c8);
-        }
-        *reinterpret_cast<u32x4*>(&sm.k[kr * AttnSmem<D>::kKStride + c8]) = kv;
-        const uint16_t* vh = reinterpret_cast<const uint16_t*>(&vv);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sm.vt[(c8 + e) * AttnSmem<D>::kVStride + kr] = vh[e];
-      }
-    } else {
-      // tree keys: rotate k at position P + depth, round to fp16; copy v.
-      // Thread handles (key kr, 8 rotation pairs starting at c8 < D/2).
-      constexpr int kPairVecs = HALF / 8;
-      for (int idx = threadIdx.x; idx < kKeyTile * kPairVecs; idx += 256) {
-        const int kr = idx / kPairVecs, c8 = (idx % kPairVecs) * 8;
-        u32x4 k1 = {0, 0, 0, 0}, k2 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0}, v2 = {0, 0, 0, 0};
-        if (kr < a.T) {
-          const uint16_t* ks = a.k + (size_t)kr * a.ldkv + g * D;
-          const uint16_t* vs = a.v + (size_t)kr * a.ldkv + g * D;
-          u32x4 r1 = *reinterpret_cast<const u32x4*>(ks + c8);
-          u32x4 r2 = *reinterpret_cast<const u32x4*>(ks + c8 + HALF);
-          v1 = *reinterpret_cast<const u32x4*>(vs + c8);
-          v2 = *reinterpret_cast<const u32x4*>(vs + c8 + HALF);
-          const float* cs = a.rope + (size_t)(P + sm.depth[kr]) * D;
-          half8 h1 = bitcast<half8>(r1), h2 = bitcast<half8>(r2), o1, o2;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float c = cs[2 * (c8 + e)], s = cs[2 * (c8 + e) + 1];
-            const float x1 = (float)h1[e], x2 = (float)h2[e];
-            o1[e] = (_Float16)(x1 * c - x2 * s);
-            o2[e] = (_Float16)(x2 * c + x1 * s);
-          }
-          k1 = bitcast<u32x4>(o1);
-          k2 = bitcast<u32x4>(o2);
-          if (rb == 0) {
-            uint16_t* kd = a.k_cache + ((size_t)g * a.S_max + P + kr) * D;
-            uint16_t* vd = a.v_cache + ((size_t)g * a.S_max + P + kr) * D;
-            *reinterpret_cast<u32x4*>(kd + c8) = k1;
-            *reinterpret_cast<u32x4*>(kd + c8 + HALF) = k2;
-            *reinterpret_cast<u32x4*>(vd + c8) = v1;
-            *reinterpret_cast<u32x4*>(vd + c8 + HALF) = v2;
-          }
-        }
-        *reinterpret_cast<u32x4*>(&sm.k[kr * AttnSmem<D>::kKStride + c8]) = k1;
-        *reinterpret_cast<u32x4*>(&sm.k[kr * AttnSmem<D>::kKStride + c8 + HALF]) = k2;
-        const uint16_t* vh1 = reinterpret_cast<const uint16_t*>(&v1);
-        const uint16_t* vh2 = reinterpret_cast<const uint16_t*>(&v2);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          sm.vt[(c8 + e) * AttnSmem<D>::kVStride + kr] = vh1[e];
-          sm.vt[(c8 + HALF + e) * AttnSmem<D>::kVStride + kr] = vh2[e];
-        }
-      }
-    }
-    __syncthreads();
-
-    // ---- S^T = K . Q^T for the tile's 4 key subtiles ----
+  // ---- one 64-key tile from LDS slot `slot`: scores, mask, softmax, P.V ----
+  auto compute = [&](int slot, int key_end, bool masked) {
     f32x4 s[4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       f32x4 c = {0.f, 0.f, 0.f, 0.f};
-      const uint16_t* krow = &sm.k[(st * 16 + n16) * AttnSmem<D>::kKStride + 8 * kq];
+      const uint16_t* krow = &ks[slot][(st * 16 + n16) * KST + 8 * kq];
 #pragma unroll
       for (int j = 0; j < KS; ++j) {
         half8 kf = *reinterpret_cast<const half8*>(krow + 32 * j);
@@ -233,9 +175,6 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
       }
       s[st] = c;  // lane: keys st*16 + 4*kq + r (r < 4), query row n16
     }
-    // ---- mask, online softmax (base 2) ----
-    const int key_end = tree_split ? a.T : (k_hi - key0);
-    const uint64_t anc = sm.anc[node];
     float tmax = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
@@ -243,7 +182,7 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int kr = st * 16 + 4 * kq + r;
         bool ok = kr < key_end;
-        if (tree_split) ok = ok && ((anc >> kr) & 1ull);
+        if (masked) ok = ok && ((anc >> kr) & 1ull);
         const float v = ok ? s[st][r] * a.scale_log2 : -INFINITY;
         s[st][r] = v;
         tmax = fmaxf(tmax, v);
@@ -251,14 +190,14 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
     const float m_new = fmaxf(m_run, tmax);
-    const float alpha = (m_new == -INFINITY) ? 1.f : exp2_approx(m_run - m_new);
+    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
     float psum = 0.f;
     half8 pf[2];
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = (s[st][r] == -INFINITY) ? 0.f : exp2_approx(s[st][r] - m_new);
+        const float p = (s[st][r] == -INFINITY) ? 0.f : exp2f(s[st][r] - m_new);
         psum += p;
         pf[st >> 1][(st & 1) * 4 + r] = (_Float16)p;
       }
@@ -273,106 +212,229 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) o[dt][r] *= ar;
     }
-    // ---- O += P . V; keys of pair pp: subtiles 2pp and 2pp+1 ----
+    // O += P . V.  A-slot 8 kq + 4 h + r of pf[pp] holds key 32 pp + 16 h +
+    // 4 kq + r; the B fragment of d-tile dt needs V[that key][16 dt + n16],
+    // i.e. two transpose reads of 4 consecutive keys (h = 0, 1), for which
+    // this lane addresses key kb + n16 / 4, columns 16 dt + 4 (n16 % 4) + 0..3.
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t* vrow = &sm.vt[(dt * 16 + n16) * AttnSmem<D>::kVStride];
-        u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + (2 * pp) * 16 + 4 * kq);
-        u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + (2 * pp + 1) * 16 + 4 * kq);
-        half8 vf = bitcast<half8>(u32x4{lo[0], lo[1], hi[0], hi[1]});
+        v4i16 hv[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int kb = 32 * pp + 16 * h + 4 * kq + (n16 >> 2);
+          const uint16_t* pv = &vs[slot][kb * KST + 16 * dt + 4 * (n16 & 3)];
+          hv[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4i16*)(pv));
+        }
+        const half8 vf = bitcast<half8>(u32x4{bitcast<u32x2>(hv[0])[0], bitcast<u32x2>(hv[0])[1],
+                                              bitcast<u32x2>(hv[1])[0], bitcast<u32x2>(hv[1])[1]});
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[pp], vf, o[dt], 0, 0, 0);
       }
     }
+  };
+
+  if (tree_split) {
+    // tree keys: rotate k at position P + depth, round to fp16; copy v.
+    // Thread handles (key kr, 8 rotation pairs starting at c8 < D/2).
+    constexpr int kPairVecs = HALF / 8;
+    for (int idx = tid; idx < kKeyTile * kPairVecs; idx += NT) {
+      const int kr = idx / kPairVecs, c8 = (idx % kPairVecs) * 8;
+      u32x4 k1 = {0, 0, 0, 0}, k2 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0}, v2 = {0, 0, 0, 0};
+      if (kr < a.T) {
+        const uint16_t* ksrc = a.k + (size_t)kr * a.ldkv + g * D;
+        const uint16_t* vsrc = a.v + (size_t)kr * a.ldkv + g * D;
+        u32x4 r1 = *reinterpret_cast<const u32x4*>(ksrc + c8);
+        u32x4 r2 = *reinterpret_cast<const u32x4*>(ksrc + c8 + HALF);
+        v1 = *reinterpret_cast<const u32x4*>(vsrc + c8);
+        v2 = *reinterpret_cast<const u32x4*>(vsrc + c8 + HALF);
+        const float* cs = a.rope + (size_t)(P + s_depth[kr]) * D;
+        half8 h1 = bitcast<half8>(r1), h2 = bitcast<half8>(r2), o1, o2;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float c = cs[2 * (c8 + e)], sn = cs[2 * (c8 + e) + 1];
+          const float x1 = (float)h1[e], x2 = (float)h2[e];
+          o1[e] = (_Float16)(x1 * c - x2 * sn);
+          o2[e] = (_Float16)(x2 * c + x1 * sn);
+        }
+        k1 = bitcast<u32x4>(o1);
+        k2 = bitcast<u32x4>(o2);
+        if (rb == 0) {
+          uint16_t* kd = a.k_cache + ((size_t)g * a.S_max + P + kr) * D;
+          uint16_t* vd = a.v_cache + ((size_t)g * a.S_max + P + kr) * D;
+          *reinterpret_cast<u32x4*>(kd + c8) = k1;
+          *reinterpret_cast<u32x4*>(kd + c8 + HALF) = k2;
+          *reinterpret_cast<u32x4*>(vd + c8) = v1;
+          *reinterpret_cast<u32x4*>(vd + c8 + HALF) = v2;
+        }
+      }
+      *reinterpret_cast<u32x4*>(&ks[0][kr * KST + c8]) = k1;
+      *reinterpret_cast<u32x4*>(&ks[0][kr * KST + c8 + HALF]) = k2;
+      *reinterpret_cast<u32x4*>(&vs[0][kr * KST + c8]) = v1;
+      *reinterpret_cast<u32x4*>(&vs[0][kr * KST + c8 + HALF]) = v2;
+    }
     __syncthreads();
-  }
-
-  // ---- publish this split's partial ----
-  const int nparts = a.nsplit + 1;
-  const size_t grp = (size_t)g * a.RB + rb;
-  const size_t part_stride = (size_t)4 * DT * kWave * 4 + 4 * 16 * 2;  // floats per workgroup partial
-  float* mine = a.part + (grp * nparts + sp) * part_stride;
+    compute(0, a.T, true);
+  } else {
+    // ---- prefix chunk of this split ----
+    const int per = (P + a.nsplit - 1) / a.nsplit;
+    const int chunk = ((per + kKeyTile - 1) / kKeyTile) * kKeyTile;
+    const int k_lo = min(P, sp * chunk);
+    const int k_hi = min(P, k_lo + chunk);
+    const int ntiles = (k_hi - k_lo + kKeyTile - 1) / kKeyTile;
+    if (ntiles > 0) {
+      const uint16_t* kc = a.k_cache + (size_t)g * a.S_max * D;
+      const uint16_t* vc = a.v_cache + (size_t)g * a.S_max * D;
+      u32x4 kr[kAttnRing][NV], vr[kAttnRing][NV];
+      // tile t (clamped to the chunk's last; rows past k_hi repeat row
+      // k_hi - 1 and are masked)
+      auto load_tile = [&](int t, u32x4 (&kd)[NV], u32x4 (&vd)[NV]) {
+        int tt = t < ntiles ? t : ntiles - 1;
+        asm volatile("" : "+s"(tt));
+        const int key0 = k_lo + tt * kKeyTile;
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) store_agent_f32x4(mine + ((size_t)(wave * DT + dt) * kWave + lane) * 4, o[dt]);
-  float* ml = mine + (size_t)4 * DT * kWave * 4;
-  if (kq == 0) {
-    store_agent_u64(ml + (wave * 16 + n16) * 2, bitcast<uint64_t>(f32x2{m_run, l_run}));
-  }
-  wait_all_memory();
-  __syncthreads();
-  uint32_t* counter = ws_counters(a.ws) + grp;
-  if (threadIdx.x == 0) sm.ticket = take_ticket(counter);
-  __syncthreads();
-  if (sm.ticket != (uint32_t)(nparts - 1)) return;
-
-  // ---- last arrival: merge the partials in split order ----
-  float mrow[4];
+        for (int j = 0; j < NV; ++j) {
+          const int idx = tid + j * NT;
+          const int key = min(key0 + idx / VPR, k_hi - 1);
+          const int c8 = (idx % VPR) * 8;
+          kd[j] = *reinterpret_cast<const u32x4*>(kc + (size_t)key * D + c8);
+          vd[j] = *reinterpret_cast<const u32x4*>(vc + (size_t)key * D + c8);
+        }
+      };
+      auto store_tile = [&](int slot, const u32x4 (&kd)[NV], const u32x4 (&vd)[NV]) {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) mrow[r] = -INFINITY;
-  const float* base = a.part + grp * nparts * part_stride;
-  for (int s2 = 0; s2 < nparts; ++s2) {
-    const float* mlp = base + s2 * part_stride + (size_t)4 * DT * kWave * 4;
+        for (int j = 0; j < NV; ++j) {
+          const int idx = tid + j * NT;
+          const int off = (idx / VPR) * KST + (idx % VPR) * 8;
+          *reinterpret_cast<u32x4*>(&ks[slot][off]) = kd[j];
+          *reinterpret_cast<u32x4*>(&vs[slot][off]) = vd[j];
+        }
+      };
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      f32x2 v2 = bitcast<f32x2>(load_agent_u64(mlp + (wave * 16 + 4 * kq + r) * 2));
-      mrow[r] = fmaxf(mrow[r], v2[0]);
-    }
-  }
-  float lsum[4] = {0.f, 0.f, 0.f, 0.f};
-  f32x4 acc[DT];
+      for (int j = 0; j < kAttnRing - 1; ++j) load_tile(j, kr[j], vr[j]);
+      store_tile(0, kr[0], vr[0]);
+      // step t: load tile t + 4, write tile t + 1 to LDS slot (t + 1) % 3
+      // (last read at step t - 2), barrier, compute tile t; whole rounds of
+      // five steps, steps past the end only load (the first one leaves)
+      for (int t0 = 0; t0 < ntiles; t0 += kAttnRing) {
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int s2 = 0; s2 < nparts; ++s2) {
-    const float* src = base + s2 * part_stride;
-    const float* mlp = src + (size_t)4 * DT * kWave * 4;
-    float w[4];
+        for (int J = 0; J < kAttnRing; ++J) {
+          const int t = t0 + J;
+          load_tile(t + kAttnRing - 1, kr[(J + kAttnRing - 1) % kAttnRing], vr[(J + kAttnRing - 1) % kAttnRing]);
+          if (t < ntiles) {
+            if (t + 1 < ntiles) store_tile((t + 1) % kAttnLds, kr[(J + 1) % kAttnRing], vr[(J + 1) % kAttnRing]);
+            lds_barrier();
+            compute(t % kAttnLds, k_hi - (k_lo + t * kKeyTile), false);
+          } else {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      f32x2 v2 = bitcast<f32x2>(load_agent_u64(mlp + (wave * 16 + 4 * kq + r) * 2));
-      w[r] = (v2[0] == -INFINITY) ? 0.f : exp2_approx(v2[0] - mrow[r]);
-      lsum[r] += w[r] * v2[1];
-    }
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      f32x4 ov = load_agent_f32x4(src + ((size_t)(wave * DT + dt) * kWave + lane) * 4);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[dt][r] += w[r] * ov[r];
-    }
-  }
-  if (threadIdx.x == 0) reset_counter(counter);
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int orow = rb * 64 + wave * 16 + 4 * kq + r;
-    if (orow < a.R) {
-      const int i = orow / a.G, qh = g * a.G + orow % a.G;
-      const float inv = 1.0f / lsum[r];
-      uint16_t* dst = a.out + (size_t)i * a.ldo + qh * D;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t h = f2h(acc[dt][r] * inv);
-        dst[dt * 16 + n16] = h;
-        if (a.out_prep) store_prepared(a.out_prep, i, qh * D + dt * 16 + n16, (a.Hq * D) >> 7, h);
+            for (int j = 0; j < NV; ++j) asm volatile("" : : "v"(kr[J][j]), "v"(vr[J][j]));
+          }
+        }
       }
     }
   }
+
+  // ---- publish this split's partial (merged by the next kernel) ----
+  float inv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float lr = __shfl(l_run, 4 * kq + r, kWave);
+    inv[r] = lr > 0.f ? 1.0f / lr : 0.f;
+  }
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    const uint32_t lo = (uint32_t)f2h(o[dt][0] * inv[0]) | ((uint32_t)f2h(o[dt][1] * inv[1]) << 16);
+    const uint32_t hi = (uint32_t)f2h(o[dt][2] * inv[2]) | ((uint32_t)f2h(o[dt][3] * inv[3]) << 16);
+    *reinterpret_cast<u32x2*>(mine + ((size_t)(wave * DT + dt) * kWave + lane) * 8) = u32x2{lo, hi};
+  }
+  if (kq == 0) *reinterpret_cast<f32x2*>(ml + (wave * 16 + n16) * 2) = f32x2{m_run, l_run};
 }
+
+// Merge of the S + 1 partials of one 16-row x 16-column output tile in
+// split order: running (max, sum) and O (partial rows times their sums)
+// rescaled to the running max.  All loads of up to 16 splits are issued
+// together (the kernel is a few memory round trips long).  Grid = Hkv x RB
+// x W x D/16, one wave each (lane: rows 4 (lane / 16) + r, column
+// lane % 16).  A row with no key at all (only possible when the attention
+// kernel rejected the tree or the prefix and published empty partials) is
+// not written.
+template <int D, int W>
+__global__ __launch_bounds__(64) void tree_attention_merge_kernel(AttnArgs a) {
+  constexpr int DT = D / 16;
+  constexpr int kBatch = 16;
+  const int lane = lane_id();
+  const int n16 = lane & 15, kq = lane >> 4;
+  const int dt = blockIdx.x % DT;
+  const int wave = (blockIdx.x / DT) % W;
+  const int grp = blockIdx.x / (DT * W);  // g * RB + rb
+  const int g = grp / a.RB, rb = grp % a.RB;
+  const int nparts = a.nsplit + 1;
+  const size_t part_stride = attn_part_bytes<D>(W);
+  const char* base = reinterpret_cast<const char*>(a.part) + (size_t)grp * nparts * part_stride;
+  float mrun[4], lrun[4];
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int r = 0; r < 4; ++r) mrun[r] = -INFINITY, lrun[r] = 0.f;
+  for (int s0 = 0; s0 < nparts; s0 += kBatch) {
+    f32x2 mlr[kBatch];  // (max, sum) of row n16 of this wave
+    u32x2 ov[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int s2 = s0 + j < nparts ? s0 + j : nparts - 1;
+      const char* src = base + s2 * part_stride;
+      const float* mlp = reinterpret_cast<const float*>(src + (size_t)W * DT * kWave * 8);
+      mlr[j] = *reinterpret_cast<const f32x2*>(mlp + (wave * 16 + n16) * 2);
+      ov[j] = *reinterpret_cast<const u32x2*>(src + ((size_t)(wave * DT + dt) * kWave + lane) * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (s0 + j >= nparts) break;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float mp = __shfl(mlr[j][0], 4 * kq + r, kWave);
+        const float lp0 = __shfl(mlr[j][1], 4 * kq + r, kWave);
+        const float m_new = fmaxf(mrun[r], mp);
+        const float w_old = (mrun[r] == -INFINITY) ? 0.f : exp2f(mrun[r] - m_new);
+        const float w_new = (mp == -INFINITY) ? 0.f : exp2f(mp - m_new);
+        const float lp = lp0 * w_new;
+        const float on = h2f((uint16_t)(ov[j][r >> 1] >> (16 * (r & 1))));
+        lrun[r] = lrun[r] * w_old + lp;
+        acc[r] = acc[r] * w_old + on * lp;
+        mrun[r] = m_new;
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int orow = rb * (16 * W) + wave * 16 + 4 * kq + r;
+    if (orow < a.R && lrun[r] > 0.f) {
+      const int i = orow / a.G, qh = g * a.G + orow % a.G;
+      const uint16_t h = f2h(acc[r] / lrun[r]);
+      a.out[(size_t)i * a.ldo + qh * D + dt * 16 + n16] = h;
+      if (a.out_prep) store_prepared(a.out_prep, i, qh * D + dt * 16 + n16, (a.Hq * D) >> 7, h);
+    }
+  }
+}
+
+static int attn_waves(int R) { return R >= 128 ? 8 : 4; }
 
 AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max) {
   AttnPlan p;
   const int G = Hq / Hkv;
   const int R = T * G;
-  const int RB = (R + 63) / 64;
+  const int W = attn_waves(R);
+  const int RB = (R + 16 * W - 1) / (16 * W);
   const int groups = Hkv * RB;
-  // about 256 workgroups in flight, at least one key tile per prefix split
+  // about 256 workgroups in flight, at least four key tiles per prefix split
   int ns = 256 / groups - 1;
   const int max_tiles = (S_max - T + kKeyTile - 1) / kKeyTile;
-  if (ns > max_tiles) ns = max_tiles;
+  if (ns > max_tiles / 4) ns = max_tiles / 4;
   if (ns < 1) ns = 1;
   p.nsplit = ns;
   p.chunk = 0;
-  const size_t part_stride = (size_t)4 * (D / 16) * kWave * 4 + 4 * 16 * 2;
-  p.part_bytes = (size_t)groups * (ns + 1) * part_stride * sizeof(float);
+  const size_t part_stride = D == 64 ? attn_part_bytes<64>(W) : attn_part_bytes<128>(W);
+  p.part_bytes = (size_t)groups * (ns + 1) * part_stride;
   return p;
 }
 
@@ -399,12 +461,29 @@ void launch_tree_attention(const AttnLaunch& L, hipStream_t st) {
   a.Hkv = L.Hkv;
   a.G = L.Hq / L.Hkv;
   a.R = L.T * a.G;
-  a.RB = (a.R + 63) / 64;
+  const int W = attn_waves(a.R);
+  a.RB = (a.R + 16 * W - 1) / (16 * W);
   a.nsplit = L.nsplit;
   a.scale_log2 = L.scale * 1.4426950408889634f;
   const dim3 grid(L.Hkv * a.RB * (L.nsplit + 1));
-  if (L.D == 64) hipLaunchKernelGGL(tree_attention_kernel<64>, grid, dim3(256), 0, st, a);
-  else hipLaunchKernelGGL(tree_attention_kernel<128>, grid, dim3(256), 0, st, a);
+  const dim3 mgrid(L.Hkv * a.RB * W * (L.D / 16));
+  if (W == 8) {
+    if (L.D == 64) {
+      hipLaunchKernelGGL((tree_attention_kernel<64, 8>), grid, dim3(512), 0, st, a);
+      hipLaunchKernelGGL((tree_attention_merge_kernel<64, 8>), mgrid, dim3(64), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((tree_attention_kernel<128, 8>), grid, dim3(512), 0, st, a);
+      hipLaunchKernelGGL((tree_attention_merge_kernel<128, 8>), mgrid, dim3(64), 0, st, a);
+    }
+  } else {
+    if (L.D == 64) {
+      hipLaunchKernelGGL((tree_attention_kernel<64, 4>), grid, dim3(256), 0, st, a);
+      hipLaunchKernelGGL((tree_attention_merge_kernel<64, 4>), mgrid, dim3(64), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((tree_attention_kernel<128, 4>), grid, dim3(256), 0, st, a);
+      hipLaunchKernelGGL((tree_attention_merge_kernel<128, 4>), mgrid, dim3(64), 0, st, a);
+    }
+  }
 }
 
 }  // namespace ss

@@ -31,11 +31,10 @@
 //     holds a weight prefetch behind an older activation load; the
 //     activations pass through a 3-slot LDS ring shared by the 4 waves, with
 //     one fence-free barrier per group.  An N-block split between
-//     workgroups is published as agent-scope partials; after its range, a
-//     workgroup takes one ticket per split N-block and the last contributor
-//     sums all partials in workgroup order: results are deterministic.
-//     Consecutive ranges are placed on the same XCD (blockIdx % 8 selects
-//     the XCD under round-robin dispatch) so split N-blocks stay on one L2.
+//     workgroups is published as fp32 partials; a fix-up kernel on the same
+//     stream sums them in workgroup order (results are deterministic) and
+//     runs the epilogue.  Consecutive ranges are placed on the same XCD
+//     (blockIdx % 8 selects the XCD under round-robin dispatch).
 #include "ss_device.h"
 #include "ss_internal.h"
 
@@ -77,81 +76,88 @@ struct BStage {
   uint32_t sz[NWV];
 };
 
-// Workgroup barrier without a memory fence: s_barrier after the wave's own
-// LDS traffic has completed.  __syncthreads() would also wait for every
-// outstanding global load (the weight prefetches); the empty asm statements
-// with a memory clobber keep the compiler from moving LDS accesses across.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
+// Kernel shapes.  R = register-ring depth (groups whose loads are in flight
+// or waiting to be used), OCC = waves per SIMD the register budget is cut
+// for.  Measured on the Llama-3-70B layer: a shallow ring with three waves
+// per SIMD (768 workgroups) suits the long SwiGLU stream, four groups at two
+// waves per SIMD (512 workgroups) the shorter projections; above 32 rows the
+// accumulators take the registers (one workgroup per CU).
+struct GemmShape {
+  int ring, occ, nwg;
+};
+constexpr GemmShape gemm_shape(int MT, bool swiglu) {
+  return MT > 2 ? GemmShape{4, 1, 256} : swiglu ? GemmShape{3, 3, 768} : GemmShape{4, 2, 512};
 }
-
-// Register-ring depth (groups whose loads are in flight or waiting to be
-// used): 6 up to 32 rows; 4 above, where the accumulators and activation
-// fragments take the registers.
-template <int MT>
-constexpr int ring_depth() { return MT <= 2 ? 6 : 4; }
 constexpr int kRingL = 3;  // LDS ring of activation fragments
 
 // Output epilogue of one N-block from the accumulators of wave `wave`
 // (kColW column tiles, for SwiGLU followed by the matching up tiles): lane
-// holds rows 4 * (lane / 16) + r of column lane % 16 of each tile.
+// holds rows 4 * (lane / 16) + r of column lane % 16 of each tile.  The
+// residual is read first (load_residual) so that its loads can overlap
+// other loads of the caller.
 template <int MT, int NWV, int EPI>
-__device__ __forceinline__ void emit_block(const GemmArgs& a, int nb, int wave, int lane,
-                                           const f32x4 (&acc)[MT][NWV]) {
-  constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;
-  constexpr int kColB = 4 * kColW;
-  const int ncol = lane & 15, kq = lane >> 4;
-  const int col0 = (nb * kColB + wave * kColW) * 16;
-  const int G2 = a.N >> 7;
-  // residual rows are all loaded before the first is used (rows >= M read
-  // row 0 and are discarded)
+struct Epilogue {
+  static constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;
+  static constexpr int kColB = 4 * kColW;
   float rv[MT][kColW][4];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int ct = 0; ct < kColW; ++ct)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) rv[mt][ct][r] = 0.f;
-  if (EPI == EPI_PLAIN && a.res) {
+
+  __device__ __forceinline__ void load_residual(const GemmArgs& a, int nb, int wave, int lane) {
+    const int ncol = lane & 15, kq = lane >> 4;
+    const int col0 = (nb * kColB + wave * kColW) * 16;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int ct = 0; ct < kColW; ++ct)
 #pragma unroll
+        for (int r = 0; r < 4; ++r) rv[mt][ct][r] = 0.f;
+    if (EPI == EPI_PLAIN && a.res) {
+      // rows >= M read row 0 and are discarded
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < kColW; ++ct)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = mt * 16 + kq * 4 + r;
+            rv[mt][ct][r] = h2f(a.res[(size_t)(m < a.M ? m : 0) * a.ldr + col0 + ct * 16 + ncol]);
+          }
+    }
+  }
+
+  __device__ __forceinline__ void write(const GemmArgs& a, int nb, int wave, int lane,
+                                        const f32x4 (&acc)[MT][NWV]) const {
+    const int ncol = lane & 15, kq = lane >> 4;
+    const int col0 = (nb * kColB + wave * kColW) * 16;
+    const int G2 = a.N >> 7;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int ct = 0; ct < kColW; ++ct) {
+        const int ncl = col0 + ct * 16 + ncol;
+#pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = mt * 16 + kq * 4 + r;
-          rv[mt][ct][r] = h2f(a.res[(size_t)(m < a.M ? m : 0) * a.ldr + col0 + ct * 16 + ncol]);
-        }
-  }
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int ct = 0; ct < kColW; ++ct) {
-      const int ncl = col0 + ct * 16 + ncol;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = mt * 16 + kq * 4 + r;
-        if (m < a.M) {
-          float val;
-          if (EPI == EPI_SWIGLU) {
-            const float gte = acc[mt][ct][r], up = acc[mt][ct + kColW][r];
-            val = gte / (1.0f + __expf(-gte)) * up;
-          } else {
-            val = acc[mt][ct][r] + rv[mt][ct][r];
+          if (m < a.M) {
+            float val;
+            if (EPI == EPI_SWIGLU) {
+              const float gte = acc[mt][ct][r], up = acc[mt][ct + kColW][r];
+              val = gte / (1.0f + __expf(-gte)) * up;
+            } else {
+              val = acc[mt][ct][r] + rv[mt][ct][r];
+            }
+            const uint16_t h = f2h(val);
+            if (a.y) a.y[(size_t)m * a.ldy + ncl] = h;
+            if (a.yp) store_prepared(a.yp, m, ncl, G2, h);
           }
-          const uint16_t h = f2h(val);
-          if (a.y) a.y[(size_t)m * a.ldy + ncl] = h;
-          if (a.yp) store_prepared(a.yp, m, ncl, G2, h);
         }
       }
-    }
-}
+  }
+};
 
 // Partial-sum slots: workgroup v publishes the accumulators of its range's
 // first (slot 0) and last (slot 1) N-block when another range shares them;
-// per slot, wave w's MT x kColW x kSrc fragments of 64 lanes x f32x4.
+// per slot, wave w's MT x kColW x kSrc fragments of 64 lanes x f32x4.  Plain
+// stores and loads: the fix-up runs in the next kernel on the stream.
 template <int MT, int NWV, int EPI>
 __device__ __forceinline__ float* part_slot(const GemmArgs& a, int v, int slot, int wave) {
   constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;
@@ -161,11 +167,12 @@ __device__ __forceinline__ float* part_slot(const GemmArgs& a, int v, int slot, 
 }
 
 template <int MT, int NWV, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT <= 2 ? 2 : 1))) void w4a16_gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(gemm_shape(MT, EPI == EPI_SWIGLU).occ)))
+void w4a16_gemm_kernel(GemmArgs a) {
   constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;  // output column tiles per wave
   constexpr int kColB = 4 * kColW;                             // output column tiles per block
   constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;
-  constexpr int kRing = ring_depth<MT>();
+  constexpr int kRing = gemm_shape(MT, EPI == EPI_SWIGLU).ring;
   __shared__ u32x4 abuf[kRingL][MT][4][kWave];  // activation fragments of 3 groups
 
   const int tid = threadIdx.x;
@@ -266,7 +273,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT <= 2 ? 2
     }
   };
 
-  auto emit = [&](int nb) { emit_block<MT, NWV, EPI>(a, nb, wave, lane, acc); };
+  auto emit = [&](int nb) {
+    Epilogue<MT, NWV, EPI> ep;
+    ep.load_residual(a, nb, wave, lane);
+    ep.write(a, nb, wave, lane, acc);
+  };
   auto zero_acc = [&]() {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -291,9 +302,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT <= 2 ? 2
 #pragma unroll
         for (int ct = 0; ct < kColW; ++ct) {
           const int t = mt * kColW + ct;
-          store_agent_f32x4(mine + ((size_t)(t * kSrc) * kWave + lane) * 4, acc[mt][ct]);
+          *reinterpret_cast<f32x4*>(mine + ((size_t)(t * kSrc) * kWave + lane) * 4) = acc[mt][ct];
           if (EPI == EPI_SWIGLU)
-            store_agent_f32x4(mine + ((size_t)(t * kSrc + 1) * kWave + lane) * 4, acc[mt][ct + kColW]);
+            *reinterpret_cast<f32x4*>(mine + ((size_t)(t * kSrc + 1) * kWave + lane) * 4) = acc[mt][ct + kColW];
         }
     }
     zero_acc();
@@ -358,6 +369,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT <= 2 ? 2
 // outputs; N-blocks inside one range were written by the GEMM kernel.
 template <int MT, int NWV, int EPI>
 __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
+  constexpr int kBatch = 8;
   constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;
   constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;
   const int nb = blockIdx.x;
@@ -368,16 +380,18 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
   if (c_first == c_last) return;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  Epilogue<MT, NWV, EPI> ep;
+  ep.load_residual(a, nb, wave, lane);  // in flight with the first partial loads
   f32x4 acc[MT][NWV];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int c0 = c_first; c0 <= c_last; c0 += 4) {
-    // four contributors' loads in flight at once, summed in order
-    f32x4 pa[4][MT][kColW], pb[4][MT][kColW];
+  for (int c0 = c_first; c0 <= c_last; c0 += kBatch) {
+    // kBatch contributors' loads in flight at once, summed in order
+    f32x4 pa[kBatch][MT][kColW], pb[kBatch][MT][kColW];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBatch; ++j) {
       const int c = c0 + j <= c_last ? c0 + j : c_last;
       const float* src = part_slot<MT, NWV, EPI>(a, c, nb == (int)(range_begin(U, c, a.nwg) / G) ? 0 : 1, wave);
 #pragma unroll
@@ -385,12 +399,12 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
 #pragma unroll
         for (int ct = 0; ct < kColW; ++ct) {
           const int t = mt * kColW + ct;
-          pa[j][mt][ct] = load_agent_f32x4(src + ((size_t)(t * kSrc) * kWave + lane) * 4);
-          if (EPI == EPI_SWIGLU) pb[j][mt][ct] = load_agent_f32x4(src + ((size_t)(t * kSrc + 1) * kWave + lane) * 4);
+          pa[j][mt][ct] = *reinterpret_cast<const f32x4*>(src + ((size_t)(t * kSrc) * kWave + lane) * 4);
+          if (EPI == EPI_SWIGLU) pb[j][mt][ct] = *reinterpret_cast<const f32x4*>(src + ((size_t)(t * kSrc + 1) * kWave + lane) * 4);
         }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kBatch; ++j) {
       if (c0 + j > c_last) break;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -401,7 +415,7 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
         }
     }
   }
-  emit_block<MT, NWV, EPI>(a, nb, wave, lane, acc);
+  ep.write(a, nb, wave, lane, acc);
 }
 
 // ------------------------------------------------------- activation prep
@@ -431,19 +445,11 @@ __global__ __launch_bounds__(256) void prepare_activations_kernel(const uint16_t
 #pragma unroll
     for (int i = 0; i < 16; ++i) a[i] = 0u;
   }
-  const _Float16 sixteen = (_Float16)16.0f;
+  u32x4 f[4];
+  pack_prepared(a, f);
+  uint16_t* base = out + (((size_t)mt * G + g) * 4) * kWave * 8;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const uint32_t* b = a + 8 * h;
-    const u32x4 lo = {(b[0] & 0xFFFFu) | (b[2] << 16), (b[1] & 0xFFFFu) | (b[3] << 16),
-                      (b[4] & 0xFFFFu) | (b[6] << 16), (b[5] & 0xFFFFu) | (b[7] << 16)};
-    const u32x4 hi = {(b[0] >> 16) | (b[2] & 0xFFFF0000u), (b[1] >> 16) | (b[3] & 0xFFFF0000u),
-                      (b[4] >> 16) | (b[6] & 0xFFFF0000u), (b[5] >> 16) | (b[7] & 0xFFFF0000u)};
-    const half8 lo16 = bitcast<half8>(lo) * sixteen;
-    uint16_t* base = out + (((size_t)mt * G + g) * 4) * kWave * 8;
-    *reinterpret_cast<u32x4*>(base + ((size_t)(h)*kWave + lane) * 8) = bitcast<u32x4>(lo16);
-    *reinterpret_cast<u32x4*>(base + ((size_t)(2 + h) * kWave + lane) * 8) = hi;
-  }
+  for (int fi = 0; fi < 4; ++fi) *reinterpret_cast<u32x4*>(base + ((size_t)fi * kWave + lane) * 8) = f[fi];
 }
 
 void launch_prepare_activations(const uint16_t* x, int M, int ldx, int K, uint16_t* out, hipStream_t st) {
@@ -554,7 +560,8 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
     p.nblocks = tiles / (4 * p.nw);
   }
   const long units = (long)p.nblocks * (K / 128);
-  p.nwg = (int)(units < kGemmWorkgroups ? units : kGemmWorkgroups);
+  const int cap = gemm_shape(MT, swiglu).nwg;
+  p.nwg = (int)(units < cap ? units : cap);
   const int col_w = swiglu ? p.nw / 2 : p.nw;
   const int src = swiglu ? 2 : 1;
   p.part_bytes = (size_t)p.nwg * 2 * 4 * MT * col_w * src * kWave * 16;

@@ -1,18 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the tree-verification step on one MI355X.
 
-A step = one Llama-3-70B-shaped decoder layer verifying a 32-token draft
-tree (8 levels, branching <= 4) over a 4096-token prefix (int4 group-128
-weights, fp16 activations and KV cache), followed by the KV commit of the
-accepted path; the whole step is one replayed HIP graph.  Inputs are seeded
-synthetic tensors already resident in HBM.  Several copies of the layer
-(weights and KV cache) are rotated so the 256 MB Infinity Cache cannot hold
-the working set.
+A step = one pass of Llama-3-70B-shaped decoder layers verifying a 32-token
+draft tree (8 levels, branching <= 4) over a 4096-token prefix (int4
+group-128 weights, fp16 activations and KV cache), replayed from one HIP
+graph.  The step runs every layer copy once (several copies of the layer's
+weights and KV cache, so the 256 MB Infinity Cache cannot hold the working
+set), and the value is per layer.  Inputs are seeded synthetic tensors
+already resident in HBM.  The KV commit of the accepted path runs once per
+model step for all layers; it is timed separately (one launch over every
+layer copy) and reported next to the per-layer value.
 
-Prints one JSON line: value = microseconds per layer-step (lower is better),
-plus the roofline of the dominant kernel (the fused SwiGLU W4A16 GEMM) timed
-on its own stream with HIP events, and the fp64 CPU reference checker timed
-on the host as a baseline.
+Prints one JSON line: value = mean microseconds per layer (lower is better)
+with p10/p50/p90 over the replays; per-operation standalone timings with
+algorithmic bytes and achieved GB/s (GEMMs with their split-K fix-up,
+attention with its merge); the roofline of the dominant operation (the
+fused SwiGLU W4A16 GEMM) timed on its own stream with HIP events; and the
+fp64 CPU reference checker timed on the host as a baseline.
 """
 import argparse
 import hashlib
@@ -114,13 +118,17 @@ def main():
     dparent = up(parent)
     dacc = up(np.array([acc], np.int32))
     host_w = {n: (w[n]["qweight"], w[n]["scales"], w[n]["zeros"]) for n in ("wqkv", "wo", "wgate", "wup", "wdown")}
+    # all copies' caches in one [copies][Hkv][S_max][D] buffer: one commit launch covers every layer
+    kc_all = up(np.broadcast_to(kc, (copies,) + kc.shape))
+    vc_all = up(np.broadcast_to(vc, (copies,) + vc.shape))
+    P_dev = up(np.array([cfg.P], np.int32))
     inst = []
     for c in range(copies):
         keep = {n: tuple(up(a) for a in host_w[n]) for n in host_w}
         w4 = {n: ss.make_w4(*keep[n]) for n in keep}
         packs = {n: ss.prepack_w4(w4[n]) for n in w4}  # kernel-native copies (one-time)
         d = {"keep": keep, "packs": packs, "w4": w4, "an": up(w["attn_norm"]), "mn": up(w["mlp_norm"]),
-             "kc": up(kc), "vc": up(vc), "P": up(np.array([cfg.P], np.int32)), "h": up(x)}
+             "kc": kc_all[c], "vc": vc_all[c], "P": P_dev, "h": up(x)}
         d["layer"] = ss.make_layer(d["an"], d["mn"], w4["wqkv"], w4["wo"], w4["wgate"], w4["wup"],
                                    w4["wdown"], d["kc"], d["vc"])
         d["ws"] = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
@@ -132,56 +140,110 @@ def main():
         run_only(args, ss, torch, np, inst, cfg, dims, dparent, dacc, rope, stream, dev)
         return
 
-    # ---------------- step graphs ----------------
-    graphs = []
+    # ---------------- step graph: every layer copy once, in order ----------------
+    # (like a multi-layer model step; the per-layer value is the step time
+    # divided by the number of layers)
+    step = ss.Graph()
     with torch.cuda.stream(stream):
+        step.begin(stream)
         for d in inst:
-            g = ss.Graph()
-            g.begin(stream)
             ss.verify_layer(d["layer"], dims, d["h"], d["P"], dparent, rope, d["ws"], stream=stream)
-            ss.kv_commit(d["kc"], d["vc"], d["P"], dparent, dacc, advance=False, ws=d["ws"], stream=stream)
-            g.end(stream)
-            graphs.append(g)
-    with torch.cuda.stream(stream):
+        step.end(stream)
         for i in range(args.warmup):
-            graphs[i % copies].launch(stream)
+            step.launch(stream)
     stream.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     with torch.cuda.stream(stream):
-        start.record(stream)
+        ev[0].record(stream)
         for i in range(args.steps):
-            graphs[i % copies].launch(stream)
-        stop.record(stream)
-    stop.synchronize()
+            step.launch(stream)
+            ev[i + 1].record(stream)
+    ev[-1].synchronize()
     torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    ms_step = ms_total / args.steps
+    ms_total = ev[0].elapsed_time(ev[-1])
+    ms_step = ms_total / args.steps / copies  # per layer
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / copies for i in range(args.steps))
+    pct = lambda q: round(per[min(len(per) - 1, int(q * len(per)))], 3)
     for d in inst:
         err = ss.read_device_error(d["ws"], stream)
         if err:
             raise RuntimeError(f"device error word {err}")
 
-    # ---------------- dominant kernel: fused SwiGLU GEMM ----------------
-    m_buf = torch.zeros((T, s.F), dtype=torch.int16, device=dev)
+    def time_op(fn, iters):
+        """Mean microseconds of one fn(i) call: `iters` calls (rotating layer
+        copies) captured into a HIP graph, replayed 3 times, timed with HIP
+        events on `stream` (no host launch overhead in the timed region)."""
+        g = ss.Graph()
+        with torch.cuda.stream(stream):
+            for i in range(3):
+                fn(i)
+            g.begin(stream)
+            for i in range(iters):
+                fn(i)
+            g.end(stream)
+            g.launch(stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                g.launch(stream)
+            e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1000.0 / (3 * iters)
+
+    # ---------------- KV commit: all layer copies in one launch ----------------
+    cm_ws = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
+    commit_us = time_op(lambda i: ss.kv_commit(kc_all, vc_all, P_dev, dparent, dacc, n_layers=copies,
+                                               advance=False, ws=cm_ws, stream=stream), 50)
+    if ss.read_device_error(cm_ws, stream):
+        raise RuntimeError("device error in kv_commit")
+
+    # ---------------- per-operation standalone timings ----------------
+    it = max(args.steps // 2, 30)
+    w4b = lambda K, N: K * N // 2 + (K // 128) * N * 3
     xin = up(x)
-    xp = torch.zeros(ss.prepared_bytes(T, s.H), dtype=torch.uint8, device=dev)
-    sw_ws = ss.workspace(ss.swiglu_workspace_bytes(T, s.H, s.F), dev)
-    sw_iters = max(args.steps, 50)
+    big_x = torch.zeros((T, max(s.H, s.F, s.Hq * s.D)), dtype=torch.int16, device=dev)
+    big_x.copy_(torch.randint(-3000, 3000, big_x.shape, dtype=torch.int16, device=dev) & 0x3BFF)
+    y = torch.zeros((T, max(s.F, s.n_qkv)), dtype=torch.int16, device=dev)
+    op_ws = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
+    preps = {K: torch.zeros(ss.prepared_bytes(T, K), dtype=torch.uint8, device=dev) for K in {s.H, s.F, s.Hq * s.D}}
     with torch.cuda.stream(stream):
-        ss.prepare_activations(xin, xp, stream=stream)
-        for i in range(5):
-            d = inst[i % copies]
-            ss.w4a16_swiglu_prepared(d["w4"]["wgate"], d["w4"]["wup"], xp, T, m_buf, sw_ws, stream=stream)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for i in range(sw_iters):
-            d = inst[i % copies]
-            ss.w4a16_swiglu_prepared(d["w4"]["wgate"], d["w4"]["wup"], xp, T, m_buf, sw_ws, stream=stream)
-        e1.record(stream)
-    e1.synchronize()
-    sw_us = e0.elapsed_time(e1) * 1000.0 / sw_iters
-    sw_bytes = 2 * (s.H * s.F // 2 + (s.H // 128) * s.F * 3)
+        for K, xp in preps.items():
+            ss.prepare_activations(big_x[:, :K], xp, stream=stream)
+    ops = {}
+
+    def gemm_op(name, wname, K, N, residual):
+        res = big_x[:, :N] if residual else None
+        us = time_op(lambda i: ss.w4a16_gemm_prepared(inst[i % copies]["w4"][wname], preps[K], T, y[:, :N],
+                                                      op_ws, residual=res, stream=stream), it)
+        ops[name] = {"us": round(us, 3), "bytes": w4b(K, N)}
+
+    gemm_op("qkv", "wqkv", s.H, s.n_qkv, False)
+    gemm_op("o_proj", "wo", s.Hq * s.D, s.H, True)
+    sw_us = time_op(lambda i: ss.w4a16_swiglu_prepared(inst[i % copies]["w4"]["wgate"], inst[i % copies]["w4"]["wup"],
+                                                       preps[s.H], T, y[:, :s.F], op_ws, stream=stream), it)
+    ops["swiglu"] = {"us": round(sw_us, 3), "bytes": 2 * w4b(s.H, s.F)}
+    gemm_op("down", "wdown", s.F, s.H, True)
+    Hd = s.Hq * s.D
+    qkv_t = big_x[:, :s.n_qkv] if s.n_qkv <= big_x.shape[1] else None
+    att_us = time_op(lambda i: ss.tree_attention(qkv_t, qkv_t[:, Hd:], qkv_t[:, Hd + s.Hkv * s.D:],
+                                                 inst[i % copies]["kc"], inst[i % copies]["vc"], P_dev, dparent,
+                                                 s.Hq, s.Hkv, s.D, rope, y[:, :Hd], op_ws, stream=stream), it)
+    att_bytes = 2 * s.Hkv * (cfg.P + T) * s.D * 2 + T * (s.n_qkv + Hd) * 2
+    ops["attention"] = {"us": round(att_us, 3), "bytes": att_bytes}
+    rn_us = time_op(lambda i: ss.rmsnorm(xin, inst[0]["an"], y[:, :s.H], stream=stream), it)
+    ops["rmsnorm"] = {"us": round(rn_us, 3), "bytes": 2 * T * s.H * 2 + s.H * 2}
+    for k, v in ops.items():
+        v["GBps"] = round(v["bytes"] / (v["us"] * 1e-6) / 1e9, 1)
+        v["frac_hbm"] = round(v["GBps"] / HBM_PEAK_GBS, 4)
+    g_names = ("qkv", "o_proj", "swiglu", "down")
+    g_bytes = sum(ops[n]["bytes"] for n in g_names)
+    g_us = sum(ops[n]["us"] for n in g_names)
+    gemm_agg = {"bytes": g_bytes, "us": round(g_us, 3), "GBps": round(g_bytes / (g_us * 1e-6) / 1e9, 1),
+                "frac_hbm": round(g_bytes / (g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    # ---------------- dominant operation: fused SwiGLU GEMM ----------------
+    sw_bytes = ops["swiglu"]["bytes"]
     sw_gbs = sw_bytes / (sw_us * 1e-6) / 1e9
     traffic = read_traffic("swiglu_gemm_c3", source_hash(GEMM_SOURCES))
 
@@ -208,7 +270,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 6),
+        "ms_per_step": round(ms_step * copies, 6),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -216,11 +278,17 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: Llama-3-70B-shaped layer, H={s.H}, Hq/Hkv={s.Hq}/{s.Hkv}, "
                                f"D={s.D}, F={s.F}, int4 g128; tree T={T} ({cfg.levels} levels, "
-                               f"branching<={cfg.branching}); prefix P={cfg.P}; verify + KV commit",
+                               f"branching<={cfg.branching}); prefix P={cfg.P}; verify_layer per step, "
+                               f"KV commit timed separately",
                    "global_batch": T, "seq_len": cfg.P + T, "parallelism": "none (1 GPU)",
-                   "layer_copies_rotated": copies},
+                   "layer_copies_rotated": copies, "layers_per_step": copies},
+        "us_per_layer_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
         "step_hbm_gbs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
-        "roofline": {"kernel": "w4a16_swiglu (gate+up, fused)", "bound": "hbm",
+        "kv_commit_us": {"all_layers": round(commit_us, 3), "layers": copies,
+                         "per_layer": round(commit_us / copies, 3)},
+        "ops": ops,
+        "gemm_aggregate": gemm_agg,
+        "roofline": {"kernel": "w4a16_swiglu (gate+up fused GEMM + split-K fix-up)", "bound": "hbm",
                      "achieved": round(sw_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(sw_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": sw_bytes, "avg_launch_us": round(sw_us, 3)},

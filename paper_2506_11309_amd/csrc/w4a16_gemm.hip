@@ -514,7 +514,9 @@ static void launch_t(const GemmLaunch& L, hipStream_t st) {
   a.units = (long)L.nblocks * a.G;
   a.part = L.part;
   hipLaunchKernelGGL((w4a16_gemm_kernel<MT, NW, EPI>), dim3(L.nwg), dim3(256), 0, st, a);
-  if (L.nwg > 1) hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks), dim3(256), 0, st, a);
+  // ranges split no N-block when every workgroup gets whole N-blocks
+  if (L.nblocks % L.nwg != 0)
+    hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks), dim3(256), 0, st, a);
 }
 
 // instantiated shapes: SwiGLU one gate + one up tile per wave; plain two

@@ -139,3 +139,24 @@ def make_tree(cfg: WorkloadConfig):
     parent = tree(cfg.T, cfg.levels, cfg.branching, seeds["tree"])
     acc = accept_leaf(parent, seeds["path"], cfg.deepest_leaf)
     return parent, acc
+
+
+def make_final_norm(cfg: WorkloadConfig):
+    """Final RMSNorm gain [H] fp16 bits (80-layer configuration)."""
+    from . import normal_f16
+    return normal_f16(cfg.seeds()["weights"], FINAL_NORM_STREAM, (cfg.shape.H,), 1.0, 0.02)
+
+
+def make_lm_head(cfg: WorkloadConfig, rows=None):
+    """LM head W [V][H] fp16 bits, N(0, 0.02); `rows` (a sequence of vocabulary
+    indices) returns just those rows, drawn from the same counter positions."""
+    import numpy as np
+    from . import normal_f16
+    H = cfg.shape.H
+    seed = cfg.seeds()["weights"]
+    if rows is None:
+        return normal_f16(seed, LM_HEAD_STREAM, (cfg.vocab, H), 0.0, 0.02)
+    out = np.empty((len(rows), H), np.uint16)
+    for i, r in enumerate(rows):
+        out[i] = normal_f16(seed, LM_HEAD_STREAM, (H,), 0.0, 0.02, offset=int(r) * H)
+    return out

@@ -246,9 +246,13 @@ size_t swiftspec_verify_layer_workspace_bytes(const swiftspec_dims* dims, int32_
  * next call that uses the workspace. */
 int swiftspec_verify_layer_workspace_layout(const swiftspec_dims* dims, int32_t T, size_t* offsets);
 
-/* Final RMSNorm and fp16 LM head: logits[m][v] = fp16( rmsnorm(h[m], gamma) . W[v] ),
- * h [M][H], W [V][H] fp16 (dense), logits [M][V].  1 <= M <= 64, H % 128 == 0,
- * V % 16 == 0. */
+/* Final RMSNorm and fp16 LM head of the verification step (the logits of
+ * every tree node, from which acceptance is decided; Sec. 3.1, Alg. 1):
+ *   logits[m][v] = fp16( xn[m] . W[v] ),  xn = fp16(rmsnorm(h[m], gamma)),
+ * fp32 accumulation.  h [M][H] fp16 (dense rows), gamma [H] fp16, W [V][H]
+ * fp16 row-major (dense, not quantised), logits [M][V] fp16 (dense rows).
+ * 1 <= M <= 64, H % 128 == 0, V % 16 == 0; pointers 16-byte aligned.  The
+ * normalised rows are kept in the workspace (after its header). */
 int swiftspec_lm_head(const uint16_t* h, int32_t M, int32_t H, const uint16_t* gamma, float eps,
                       const uint16_t* W, int32_t V, uint16_t* logits, void* ws, size_t ws_bytes,
                       void* stream);

@@ -93,4 +93,7 @@ void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc
 
 void launch_ws_init(void* ws, size_t bytes, hipStream_t st);
 
+void launch_lm_head(const uint16_t* xn, int M, int H, const uint16_t* W, int V, uint16_t* logits, int ldl,
+                    hipStream_t st);
+
 }  // namespace ss

@@ -482,18 +482,23 @@ int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, u
 }
 
 size_t swiftspec_lm_head_workspace_bytes(int32_t M, int32_t H, int32_t V) {
-  (void)M;
-  (void)H;
   (void)V;
-  return kHeader;
+  if (M < 1 || H < 1) return kHeader;
+  return kHeader + align_up((size_t)M * H * 2);
 }
 
 int swiftspec_lm_head(const uint16_t* h, int32_t M, int32_t H, const uint16_t* gamma, float eps,
                       const uint16_t* W, int32_t V, uint16_t* logits, void* ws, size_t ws_bytes,
                       void* stream) {
-  (void)h; (void)M; (void)H; (void)gamma; (void)eps; (void)W; (void)V; (void)logits; (void)ws;
-  (void)ws_bytes; (void)stream;
-  return SWIFTSPEC_UNSUPPORTED;
+  if (!h || !gamma || !W || !logits || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (M < 1 || H < 1 || V < 1) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M || H % 128 || V % 16) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(h) || !aligned16(gamma) || !aligned16(W) || !aligned16(ws)) return SWIFTSPEC_MISALIGNED;
+  if (ws_bytes < swiftspec_lm_head_workspace_bytes(M, H, V)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  uint16_t* xn = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + kHeader);
+  ss::launch_rmsnorm(h, M, H, H, gamma, eps, xn, H, nullptr, S(stream));
+  ss::launch_lm_head(xn, M, H, W, V, logits, V, S(stream));
+  return check_launch();
 }
 
 struct swiftspec_graph {

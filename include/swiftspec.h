@@ -258,6 +258,25 @@ int swiftspec_lm_head(const uint16_t* h, int32_t M, int32_t H, const uint16_t* g
                       void* stream);
 size_t swiftspec_lm_head_workspace_bytes(int32_t M, int32_t H, int32_t V);
 
+/* The target model's whole verification forward over the draft tree
+ * (Alg. 1, batch verify; Sec. 3.1): decoder layers 0 .. n_layers-1 in order
+ * (each exactly as swiftspec_verify_layer, with layers[l]'s weights and
+ * caches), then, if V > 0, the final RMSNorm and LM head
+ * (swiftspec_lm_head) into logits [T][V].  hidden [T][H] is the input
+ * embedding of the tree tokens and holds the last layer's output on return.
+ * All layers share dims, T, the device prefix length, the parent array and
+ * the RoPE table.  Every argument of every layer is checked before the
+ * first launch; nothing is enqueued if one fails.  V == 0 skips the head
+ * (final_norm, lm_head and logits may then be NULL).  One call enqueues
+ * 7 n_layers + 2 kernels (+ split fix-ups) and can be captured whole into
+ * one graph. */
+int swiftspec_verify_step(const swiftspec_layer* layers, int32_t n_layers, const swiftspec_dims* dims,
+                          uint16_t* hidden, int32_t T, const int32_t* d_prefix_len,
+                          const int32_t* d_parent, const float* rope_cos_sin,
+                          const uint16_t* final_norm, const uint16_t* lm_head, int32_t V,
+                          uint16_t* logits, void* ws, size_t ws_bytes, void* stream);
+size_t swiftspec_verify_step_workspace_bytes(const swiftspec_dims* dims, int32_t T, int32_t V);
+
 /* ---------------------------------------------------------- HIP graphs
  * Capture the calls issued on `stream` between begin and end into an
  * executable graph (hipStreamBeginCapture / hipGraphInstantiate) and replay

@@ -85,6 +85,9 @@ _SIGS = {
     "swiftspec_verify_layer_workspace_layout": ([ctypes.POINTER(Dims), i32, ctypes.POINTER(sz)], ctypes.c_int),
     "swiftspec_lm_head": ([vp, i32, i32, vp, f32, vp, i32, vp, vp, sz, vp], ctypes.c_int),
     "swiftspec_lm_head_workspace_bytes": ([i32, i32, i32], sz),
+    "swiftspec_verify_step": ([ctypes.POINTER(Layer), i32, ctypes.POINTER(Dims), vp, i32, vp, vp, vp, vp, vp,
+                               i32, vp, vp, sz, vp], ctypes.c_int),
+    "swiftspec_verify_step_workspace_bytes": ([ctypes.POINTER(Dims), i32, i32], sz),
     "swiftspec_graph_begin": ([vp], ctypes.c_int),
     "swiftspec_graph_end": ([vp, ctypes.POINTER(vp)], ctypes.c_int),
     "swiftspec_graph_launch": ([vp, vp], ctypes.c_int),
@@ -330,6 +333,29 @@ def lm_head(h, gamma, W, logits, ws, eps=1e-5, stream=None):
     st = _load().swiftspec_lm_head(_ptr(h), M, H, _ptr(gamma), eps, _ptr(W), V, _ptr(logits), _ptr(ws),
                                    ws.numel(), _stream(stream))
     _check(st, "lm_head")
+
+
+def verify_step_workspace_bytes(dims: Dims, T: int, V: int) -> int:
+    return int(_load().swiftspec_verify_step_workspace_bytes(ctypes.byref(dims), T, V))
+
+
+def make_layers(layers):
+    """A contiguous ctypes array of Layer descriptors for verify_step."""
+    arr = (Layer * len(layers))()
+    for i, l in enumerate(layers):
+        arr[i] = l
+    return arr
+
+
+def verify_step(layers, dims: Dims, hidden, prefix_len, parent, rope, ws, final_norm=None, lm_head_w=None,
+                logits=None, stream=None):
+    """All decoder layers in order, then (if lm_head_w is given) the final
+    RMSNorm and LM head into logits.  `layers` is a make_layers() array."""
+    V = 0 if lm_head_w is None else lm_head_w.shape[0]
+    st = _load().swiftspec_verify_step(layers, len(layers), ctypes.byref(dims), _ptr(hidden), hidden.shape[0],
+                                       _ptr(prefix_len), _ptr(parent), _ptr(rope), _ptr(final_norm),
+                                       _ptr(lm_head_w), V, _ptr(logits), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "verify_step")
 
 
 class Graph:

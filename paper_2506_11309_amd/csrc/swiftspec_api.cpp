@@ -441,10 +441,8 @@ int swiftspec_verify_layer_workspace_layout(const swiftspec_dims* dims, int32_t 
   return SWIFTSPEC_OK;
 }
 
-int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, uint16_t* hidden,
-                           int32_t T, const int32_t* d_prefix_len, const int32_t* d_parent,
-                           const float* rope, void* ws, size_t ws_bytes, void* stream) {
-  if (!Lw || !d || !hidden || !d_prefix_len || !d_parent || !rope || !ws) return SWIFTSPEC_INVALID_ARG;
+// Synchronous argument checks of one decoder layer (nothing is launched).
+static int check_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, int32_t T) {
   if (!Lw->attn_norm || !Lw->mlp_norm || !Lw->k_cache || !Lw->v_cache) return SWIFTSPEC_INVALID_ARG;
   if (T < 1 || d->H < 1 || d->Hq < 1 || d->Hkv < 1 || d->F < 1 || d->S_max < T) return SWIFTSPEC_INVALID_ARG;
   if (T > SWIFTSPEC_MAX_TREE || (d->D != 64 && d->D != 128) || d->Hq % d->Hkv) return SWIFTSPEC_UNSUPPORTED;
@@ -458,17 +456,23 @@ int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, u
       Lw->wgate.K != H || Lw->wgate.N != F || Lw->wup.K != H || Lw->wup.N != F ||
       Lw->wdown.K != F || Lw->wdown.N != H)
     return SWIFTSPEC_INVALID_ARG;
-  if (!aligned16(hidden) || !aligned16(Lw->attn_norm) || !aligned16(Lw->mlp_norm) ||
-      !aligned16(Lw->k_cache) || !aligned16(Lw->v_cache) || !aligned16(ws))
+  if (!aligned16(Lw->attn_norm) || !aligned16(Lw->mlp_norm) || !aligned16(Lw->k_cache) ||
+      !aligned16(Lw->v_cache))
     return SWIFTSPEC_MISALIGNED;
+  return SWIFTSPEC_OK;
+}
+
+// Enqueue one checked decoder layer on `st`.
+static void enqueue_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, uint16_t* hidden, int32_t T,
+                          const int32_t* d_prefix_len, const int32_t* d_parent, const float* rope,
+                          void* ws, hipStream_t st) {
+  const int H = d->H, Hd = d->Hq * d->D, Nqkv = (d->Hq + 2 * d->Hkv) * d->D, F = d->F;
   const LayerWs w = layer_ws(d, T);
-  if (ws_bytes < w.total) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   char* base = static_cast<char*>(ws);
   auto at = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
   uint16_t *xn = at(w.xn), *qkv = at(w.qkv), *o = at(w.o), *h = at(w.h), *hn = at(w.hn), *m = at(w.m);
   uint16_t *xn_p = at(w.xn_p), *o_p = at(w.o_p), *hn_p = at(w.hn_p), *m_p = at(w.m_p);
   float* part = reinterpret_cast<float*>(base + w.part);
-  hipStream_t st = S(stream);
   ss::launch_rmsnorm(hidden, T, H, H, Lw->attn_norm, d->eps, xn, H, xn_p, st);
   run_gemm(&Lw->wqkv, nullptr, xn_p, T, qkv, Nqkv, nullptr, nullptr, 0, ws, part, st);
   run_attention(qkv, Nqkv, qkv + Hd, qkv + Hd + d->Hkv * d->D, Nqkv, Lw->k_cache, Lw->v_cache,
@@ -478,6 +482,54 @@ int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, u
   ss::launch_rmsnorm(h, T, H, H, Lw->mlp_norm, d->eps, hn, H, hn_p, st);
   run_gemm(&Lw->wgate, &Lw->wup, hn_p, T, m, F, m_p, nullptr, 0, ws, part, st);
   run_gemm(&Lw->wdown, nullptr, m_p, T, hidden, H, nullptr, h, H, ws, part, st);
+}
+
+int swiftspec_verify_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, uint16_t* hidden,
+                           int32_t T, const int32_t* d_prefix_len, const int32_t* d_parent,
+                           const float* rope, void* ws, size_t ws_bytes, void* stream) {
+  if (!Lw || !d || !hidden || !d_prefix_len || !d_parent || !rope || !ws) return SWIFTSPEC_INVALID_ARG;
+  int rc = check_layer(Lw, d, T);
+  if (rc) return rc;
+  if (!aligned16(hidden) || !aligned16(ws)) return SWIFTSPEC_MISALIGNED;
+  if (ws_bytes < layer_ws(d, T).total) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  enqueue_layer(Lw, d, hidden, T, d_prefix_len, d_parent, rope, ws, S(stream));
+  return check_launch();
+}
+
+size_t swiftspec_verify_step_workspace_bytes(const swiftspec_dims* dims, int32_t T, int32_t V) {
+  if (!dims || T < 1 || T > SWIFTSPEC_MAX_TREE) return kHeader;
+  const size_t layer = layer_ws(dims, T).total;
+  const size_t head = V > 0 ? swiftspec_lm_head_workspace_bytes(T, dims->H, V) : 0;
+  return layer > head ? layer : head;
+}
+
+int swiftspec_verify_step(const swiftspec_layer* layers, int32_t n_layers, const swiftspec_dims* d,
+                          uint16_t* hidden, int32_t T, const int32_t* d_prefix_len,
+                          const int32_t* d_parent, const float* rope, const uint16_t* final_norm,
+                          const uint16_t* lm_head, int32_t V, uint16_t* logits, void* ws,
+                          size_t ws_bytes, void* stream) {
+  if (!layers || !d || !hidden || !d_prefix_len || !d_parent || !rope || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (n_layers < 0 || V < 0 || (n_layers == 0 && V == 0)) return SWIFTSPEC_INVALID_ARG;
+  if (T < 1) return SWIFTSPEC_INVALID_ARG;
+  if (T > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_UNSUPPORTED;
+  int rc;
+  for (int l = 0; l < n_layers; ++l)
+    if ((rc = check_layer(&layers[l], d, T))) return rc;
+  if (V > 0) {
+    if (!final_norm || !lm_head || !logits) return SWIFTSPEC_INVALID_ARG;
+    if (d->H < 1) return SWIFTSPEC_INVALID_ARG;
+    if (d->H % 128 || V % 16) return SWIFTSPEC_UNSUPPORTED;
+    if (!aligned16(final_norm) || !aligned16(lm_head)) return SWIFTSPEC_MISALIGNED;
+  }
+  if (!aligned16(hidden) || !aligned16(ws)) return SWIFTSPEC_MISALIGNED;
+  if (ws_bytes < swiftspec_verify_step_workspace_bytes(d, T, V)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  hipStream_t st = S(stream);
+  for (int l = 0; l < n_layers; ++l) enqueue_layer(&layers[l], d, hidden, T, d_prefix_len, d_parent, rope, ws, st);
+  if (V > 0) {
+    uint16_t* xn = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + kHeader);
+    ss::launch_rmsnorm(hidden, T, d->H, d->H, final_norm, d->eps, xn, d->H, nullptr, st);
+    ss::launch_lm_head(xn, T, d->H, lm_head, V, logits, V, st);
+  }
   return check_launch();
 }
 

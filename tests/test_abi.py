@@ -80,6 +80,33 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert lib.swiftspec_graph_begin(None) == ss.INVALID_ARG
 
 
+def test_verify_step_rejects_before_launch(ss):
+    lib = ss.lib()
+    fake = 0x10000  # never dereferenced: validation fails first
+    H, Hq, Hkv, D, F, S = 2048, 32, 8, 64, 8192, 1024
+    d = ss.make_dims(H, Hq, Hkv, D, F, S)
+    w = lambda K, N: ss.W4(fake, fake, fake, K, N, fake)
+    good = ss.Layer(fake, fake, w(H, (Hq + 2 * Hkv) * D), w(Hq * D, H), w(H, F), w(H, F), w(F, H), fake, fake)
+    bad = ss.Layer(fake, fake, w(H, (Hq + 2 * Hkv) * D), w(Hq * D, H), w(H, F), w(H, F), w(F, H), None, fake)
+    wrong = ss.Layer(fake, fake, w(H, (Hq + 2 * Hkv) * D), w(Hq * D, H), w(H, F), w(H, 2 * F), w(F, H), fake, fake)
+    ws = 1 << 40
+
+    def step(layers, n, V, T=8, ws_bytes=ws, logits=fake):
+        return lib.swiftspec_verify_step(ss.make_layers(layers), n, ctypes.byref(d), fake, T, fake, fake, fake,
+                                         fake, fake, V, logits, fake, ws_bytes, None)
+
+    assert step([good], 0, 0) == ss.INVALID_ARG          # nothing to do
+    assert step([good], 1, 24) == ss.UNSUPPORTED         # V % 16 != 0
+    assert step([good], 1, 32, logits=None) == ss.INVALID_ARG
+    assert step([good, bad], 2, 0) == ss.INVALID_ARG     # a later layer's null cache: nothing enqueued
+    assert step([good, wrong], 2, 0) == ss.INVALID_ARG   # a later layer's mismatched shape
+    assert step([good], 1, 32, T=65) == ss.UNSUPPORTED
+    assert step([good], 1, 32, ws_bytes=16) == ss.WORKSPACE_TOO_SMALL
+    step_ws = ss.verify_step_workspace_bytes(d, 8, 32000)
+    assert step_ws >= ss.verify_layer_workspace_bytes(d, 8)
+    assert step_ws >= lib.swiftspec_lm_head_workspace_bytes(8, H, 32000)
+
+
 def test_workspace_queries(ss):
     lib = ss.lib()
     for M, K, N in ((8, 2048, 3072), (32, 8192, 10240), (64, 28672, 8192)):

@@ -24,6 +24,7 @@ def _gpu():
 
 import paper_2506_11309_amd as ss  # noqa: E402
 from gpu_helpers import DeviceLayer, check_close, dev, down16, up  # noqa: E402
+from layer_stages import oracle_stages, split_qkv as _split_qkv  # noqa: E402
 
 
 def _oracle_dims(cfg):
@@ -31,9 +32,43 @@ def _oracle_dims(cfg):
     return {"H": s.H, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "F": s.F, "S_max": cfg.S_max}
 
 
+def gpu_stages(L_dev, src, kc, vc):
+    """Every stage of the layer through the standalone entry points, each fed
+    the given stage inputs src (host fp16 bits: x, xn, qkv, o, h, hn, m);
+    the attention runs on fresh device copies of the caches kc, vc.  Returns
+    the stage outputs and the device caches."""
+    cfg, s = L_dev.cfg, L_dev.cfg.shape
+    T, H, F, Hd = cfg.T, s.H, s.F, s.Hq * s.D
+    nb = max(ss.gemm_workspace_bytes(T, K, N) for _, K, N in s.gemms())
+    nb = max(nb, ss.swiglu_workspace_bytes(T, H, F),
+             ss.tree_attention_workspace_bytes(T, s.Hq, s.Hkv, s.D, cfg.S_max))
+    ws = ss.workspace(nb, dev())
+    new = lambda n: torch.zeros((T, n), dtype=torch.int16, device=dev())
+    d = {k: up(v) for k, v in src.items()}
+    g = {k: new(n) for k, n in (("xn", H), ("qkv", s.n_qkv), ("o", Hd), ("h", H), ("hn", H),
+                                ("m", F), ("out", H))}
+    dkc, dvc = up(kc), up(vc)
+    ss.rmsnorm(d["x"], L_dev.attn_norm, g["xn"])
+    ss.w4a16_gemm(L_dev.w4["wqkv"], d["xn"], g["qkv"], ws)
+    q, k, v = _split_qkv(s, d["qkv"])
+    ss.tree_attention(q, k, v, dkc, dvc, L_dev.P, L_dev.parent, s.Hq, s.Hkv, s.D, L_dev.rope, g["o"], ws)
+    ss.w4a16_gemm(L_dev.w4["wo"], d["o"], g["h"], ws, residual=d["x"])
+    ss.rmsnorm(d["h"], L_dev.mlp_norm, g["hn"])
+    ss.w4a16_swiglu(L_dev.w4["wgate"], L_dev.w4["wup"], d["hn"], g["m"], ws)
+    ss.w4a16_gemm(L_dev.w4["wdown"], d["m"], g["out"], ws, residual=d["h"])
+    torch.cuda.synchronize()
+    assert ss.read_device_error(ws) == 0
+    return {k: down16(t) for k, t in g.items()}, down16(dkc), down16(dvc)
+
+
+STAGES = ("xn", "qkv", "o", "h", "hn", "m", "out")
+
+
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
 def test_verify_layer_and_commit_match_oracle(name):
     cfg = CONFIGS[name]
+    s = cfg.shape
+    P, T = cfg.P, cfg.T
     w = make_layer_weights(cfg)
     kc, vc = make_kv_prefix(cfg)
     x = make_activations(cfg)
@@ -42,54 +77,70 @@ def test_verify_layer_and_commit_match_oracle(name):
     h = L_dev.run(x)
     assert ss.read_device_error(L_dev.ws) == 0
     out = down16(h)
-    mid = {k: down16(v) for k, v in ss.verify_layer_intermediates(L_dev.dims, cfg.T, L_dev.ws).items()}
-    s = cfg.shape
-    Hd = s.Hq * s.D
-    # stage by stage: each GPU stage against the reference stage applied to
-    # the GPU's own stage input, under the GEMM / attention tolerance
-    check_close(mid["xn"], oracle.rmsnorm(x, w["attn_norm"]), "attn rmsnorm")
-    check_close(mid["qkv"], oracle.w4a16_gemm(w["wqkv"], mid["xn"]), "qkv gemm")
-    skc, svc = kc.copy(), vc.copy()
-    q, k, v = (np.ascontiguousarray(mid["qkv"][:, a:b]) for a, b in
-               ((0, Hd), (Hd, Hd + s.Hkv * s.D), (Hd + s.Hkv * s.D, s.n_qkv)))
-    check_close(mid["o"], oracle.tree_attention(q, k, v, skc, svc, cfg.P, parent, s.Hq, s.Hkv, s.D),
-                "tree attention")
-    check_close(mid["h"], oracle.w4a16_gemm(w["wo"], mid["o"], residual=x), "o-proj + residual")
-    check_close(mid["hn"], oracle.rmsnorm(mid["h"], w["mlp_norm"]), "mlp rmsnorm")
-    check_close(mid["m"], oracle.w4a16_swiglu(w["wgate"], w["wup"], mid["hn"]), "swiglu")
-    check_close(out, oracle.w4a16_gemm(w["wdown"], mid["m"], residual=mid["h"]), "down + residual")
-    # end to end against the independent reference chain.  The two chains
-    # round to fp16 at the same seven storage points, but a value within
-    # rounding distance of a boundary may round differently on each side,
-    # and such one-ulp differences propagate through every later stage
-    # (e.g. through the K = F sum of the down projection).  Per-stage parity
-    # above is the kernel criterion; here the propagated difference is
-    # reported and bounded loosely to catch gross errors.
+    gk, gv = down16(L_dev.kc), down16(L_dev.vc)
+    mid = {k: down16(v) for k, v in ss.verify_layer_intermediates(L_dev.dims, T, L_dev.ws).items()}
+    mid["x"], mid["out"] = x, out
+    # 1. the fused layer is exactly the composition of the standalone
+    #    kernels: each entry point fed the layer's own stage inputs
+    #    reproduces the layer's stage output bit for bit (GPU against GPU)
+    comp, ck, cv = gpu_stages(L_dev, {k: mid[k] for k in ("x", "xn", "qkv", "o", "h", "hn", "m")}, kc, vc)
+    for k in STAGES:
+        assert np.array_equal(comp[k], mid[k]), f"{name}: fused layer differs from the standalone {k} stage"
+    assert np.array_equal(ck, gk) and np.array_equal(cv, gv)
+    # 2. stage parity against the reference: every standalone entry point
+    #    fed the REFERENCE stage inputs, against the reference stage output
     okc, ovc = kc.copy(), vc.copy()
-    ref = oracle.verify_layer(_oracle_dims(cfg), w, okc, ovc, x, cfg.P, parent)
-    g64, r64 = out.view(np.float16).astype(np.float64), ref.view(np.float16).astype(np.float64)
-    e2e = np.abs(g64 - r64)
-    rms = np.sqrt(np.mean(r64 ** 2))
+    ref = oracle_stages(cfg, w, okc, ovc, x, parent)
+    got, rk, rv = gpu_stages(L_dev, {k: ref[k] for k in ("x", "xn", "qkv", "o", "h", "hn", "m")}, kc, vc)
+    for k in STAGES:
+        err, rel = check_close(got[k], ref[k], f"{name} stage {k}")
+        print(f"{name} stage {k}: max abs err {err:.3g}, max rel err (|r|>=0.2) {rel:.3g}")
+    assert np.array_equal(rk[:, :P], okc[:, :P]) and np.array_equal(rv, ovc)  # values copied bit-exactly
+    check_close(rk[:, P:P + T], okc[:, P:P + T], "rotated tree keys")
+    # 3. end to end against the reference chain.  Both chains round to fp16
+    #    at the same seven storage points, but the attention's and GEMMs'
+    #    in-tolerance differences flip some stored values by an ulp, and the
+    #    flips propagate (e.g. a residual h of magnitude 10 carries its ulp
+    #    0.008 into an output that cancels to 0.5).  The per-stage parity
+    #    above is the kernel criterion; here the propagated difference is
+    #    reported and bounded loosely to catch gross errors.
+    r64 = ref["out"].view(np.float16).astype(np.float64)
+    e2e = np.abs(out.view(np.float16).astype(np.float64) - r64)
     print(f"{name}: end-to-end max abs err {e2e.max():.3g}, p99.9 {np.quantile(e2e, 0.999):.3g}, "
-          f"output rms {rms:.3g}, outside per-stage tolerance: "
+          f"output rms {np.sqrt(np.mean(r64 ** 2)):.3g}, outside per-stage tolerance: "
           f"{int((e2e > 2e-3 + 1e-2 * np.abs(r64)).sum())} of {e2e.size}")
     assert np.all(e2e <= 0.05 + 0.02 * np.abs(r64)), e2e.max()
-    P = cfg.P
-    gk, gv = down16(L_dev.kc), down16(L_dev.vc)
-    assert np.array_equal(gv[:, P:P + cfg.T], svc[:, P:P + cfg.T])  # values copied bit-exactly
-    check_close(gk[:, P:P + cfg.T], skc[:, P:P + cfg.T], "rotated tree keys")
-    # prefix rows untouched; tree rows hold this layer's (GPU-computed) k, v
-    assert np.array_equal(gk[:, :P], okc[:, :P]) and np.array_equal(gv[:, :P], ovc[:, :P])
-    check_close(gk[:, P:P + cfg.T], okc[:, P:P + cfg.T], "tree keys in cache")
-    check_close(gv[:, P:P + cfg.T], ovc[:, P:P + cfg.T], "tree values in cache")
-    # commit the accepted path; compare every cache element against the
-    # reference commit applied to the GPU's own cache contents (bit-exact)
+    # the layer's cache writes: prefix rows untouched, tree rows within
+    # tolerance of the reference chain's, values of its own v bit-exactly
+    assert np.array_equal(gk[:, :P], kc[:, :P]) and np.array_equal(gv[:, :P], vc[:, :P])
+    check_close(gk[:, P:P + T], okc[:, P:P + T], "tree keys in cache", atol=0.05, rtol=0.02)
+    check_close(gv[:, P:P + T], ovc[:, P:P + T], "tree values in cache", atol=0.05, rtol=0.02)
+    hv = _split_qkv(s, mid["qkv"])[2].reshape(T, s.Hkv, s.D).transpose(1, 0, 2)
+    assert np.array_equal(gv[:, P:P + T], hv)
+    # 4. commit of the accepted path, on the reference's caches, against the
+    #    reference commit (every cache element, bit-exact)
+    dk, dv = up(okc), up(ovc)
+    dP = up(np.array([P], np.int32))
     dacc = up(np.array([acc], np.int32))
+    ss.kv_commit(dk, dv, dP, L_dev.parent, dacc, advance=True, ws=L_dev.ws)
+    torch.cuda.synchronize()
+    L = oracle.kv_commit(okc, ovc, P, parent, acc)
+    assert np.array_equal(down16(dk), okc) and np.array_equal(down16(dv), ovc)
+    assert int(dP.item()) == P + L
+    # ... and on the layer's own caches: row P + i receives row P + pi_i of
+    #    the pre-commit cache (pi from the seeded parent array), the rest
+    #    keeps its bytes
+    path = [acc]
+    while path[-1] != 0:
+        path.append(int(parent[path[-1]]))
+    path = path[::-1]
     ss.kv_commit(L_dev.kc, L_dev.vc, L_dev.P, L_dev.parent, dacc, advance=True, ws=L_dev.ws)
     torch.cuda.synchronize()
-    L = oracle.kv_commit(gk, gv, P, parent, acc)
-    assert np.array_equal(down16(L_dev.kc), gk) and np.array_equal(down16(L_dev.vc), gv)
-    assert int(L_dev.P.item()) == P + L
+    ek, ev = gk.copy(), gv.copy()
+    ek[:, P:P + len(path)] = gk[:, [P + j for j in path]]
+    ev[:, P:P + len(path)] = gv[:, [P + j for j in path]]
+    assert np.array_equal(down16(L_dev.kc), ek) and np.array_equal(down16(L_dev.vc), ev)
+    assert int(L_dev.P.item()) == P + len(path) == P + L
 
 
 def test_verify_layer_deterministic_and_graph_replay_bitwise():

@@ -292,3 +292,24 @@ def test_layer_wiring_mlp_block_closed_form():
     hn = f64(oracle.rmsnorm(x, w["mlp_norm"]))
     m = f64(f16bits(hn / (1 + np.exp(-hn)) * (2 * hn)))
     assert np.array_equal(out, f16bits(f64(x) + m))
+
+
+@pytest.mark.parametrize("name", ["c1"])
+def test_layer_equals_composition_of_its_stages(name):
+    """The one-call reference layer and the stage-by-stage reference chain
+    (used for the GPU stage parity) are the same computation, bit for bit."""
+    from layer_stages import oracle_stages
+    from gen.workloads import CONFIGS, make_activations, make_kv_prefix, make_layer_weights, make_tree
+    cfg = CONFIGS[name]
+    s = cfg.shape
+    w = make_layer_weights(cfg)
+    kc, vc = make_kv_prefix(cfg)
+    x = make_activations(cfg)
+    parent, _ = make_tree(cfg)
+    dims = {"H": s.H, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "F": s.F, "S_max": cfg.S_max}
+    k1, v1 = kc.copy(), vc.copy()
+    out = oracle.verify_layer(dims, w, k1, v1, x, cfg.P, parent)
+    k2, v2 = kc.copy(), vc.copy()
+    r = oracle_stages(cfg, w, k2, v2, x, parent)
+    assert np.array_equal(out, r["out"])
+    assert np.array_equal(k1, k2) and np.array_equal(v1, v2)

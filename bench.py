@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--only-kernel", default="", help="launch only this kernel (for counter runs): "
                     "swiglu | qkv | o | down | attention | commit | copy")
     ap.add_argument("--iters", type=int, default=50)
+    ap.add_argument("--no-full-step", action="store_true",
+                    help="skip the 80-layer step (all layers + final norm + LM head) timing")
+    ap.add_argument("--full-step-reps", type=int, default=10)
     return ap.parse_args()
 
 
@@ -247,6 +250,8 @@ def main():
     sw_gbs = sw_bytes / (sw_us * 1e-6) / 1e9
     traffic = read_traffic("swiglu_gemm_c3", source_hash(GEMM_SOURCES))
 
+    full = None if args.no_full_step else full_step(args, ss, torch, np, dev, stream)
+
     # ---------------- CPU baseline: the fp64 reference checker ----------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -288,14 +293,113 @@ def main():
                          "per_layer": round(commit_us / copies, 3)},
         "ops": ops,
         "gemm_aggregate": gemm_agg,
-        "roofline": {"kernel": "w4a16_swiglu (gate+up fused GEMM + split-K fix-up)", "bound": "hbm",
+        "roofline": {"kernel": "w4a16_swiglu (gate+up fused GEMM; one workgroup per 64-column block, no split at this shape)", "bound": "hbm",
                      "achieved": round(sw_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(sw_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": sw_bytes, "avg_launch_us": round(sw_us, 3)},
         "cpu_baseline": cpu,
+        "full_step_80_layers": full,
         "input_generation_s": round(gen_s, 2),
     }
     print(json.dumps(out), flush=True)
+
+
+def full_step(args, ss, torch, np, dev, stream):
+    """The 80-layer Llama-3-70B-shaped verification step (T = 64, P = 8192,
+    final RMSNorm + fp16 LM head over 128256 rows) as one HIP graph: every
+    layer's own weights and caches (35.8 GB of int4 weights + 2.1 GB LM head
+    + 2.7 GB of KV cache, drawn on the device with the workload recipe), the
+    graph replayed `full_step_reps` times and timed with HIP events; the
+    KV commit of the accepted path over all 80 layers timed as one launch."""
+    from gen import device as gdev
+    from gen import workloads as wl
+    cfg = wl.CONFIGS["c5"]
+    s = cfg.shape
+    T, nl = cfg.T, cfg.n_layers
+    seed, kv_seed = cfg.seeds()["weights"], cfg.seeds()["kv"]
+    t0 = time.time()
+    shape = (nl, s.Hkv, cfg.S_max, s.D)
+    kc = torch.zeros(shape, dtype=torch.int16, device=dev)
+    vc = torch.zeros(shape, dtype=torch.int16, device=dev)
+    keep, descs = [], []
+    for l in range(nl):
+        base = l * wl.LAYER_STREAM_STRIDE
+        w4 = {}
+        for name, K, N in s.gemms():
+            q, sc, z = gdev.w4_random_device(seed, base + wl.W_STREAMS[name], N, K, device=dev)
+            d = ss.make_w4(q, sc, z)
+            keep.append((q, sc, z, ss.prepack_w4(d)))
+            w4[name] = d
+        an = gdev.normal_f16_device(seed, base + wl.W_STREAMS["attn_norm"], (s.H,), 1.0, 0.02, dev)
+        mn = gdev.normal_f16_device(seed, base + wl.W_STREAMS["mlp_norm"], (s.H,), 1.0, 0.02, dev)
+        kc[l, :, :cfg.P] = gdev.normal_f16_device(kv_seed, 2 * l, (s.Hkv, cfg.P, s.D), device=dev)
+        vc[l, :, :cfg.P] = gdev.normal_f16_device(kv_seed, 2 * l + 1, (s.Hkv, cfg.P, s.D), device=dev)
+        keep.append((an, mn))
+        descs.append(ss.make_layer(an, mn, w4["wqkv"], w4["wo"], w4["wgate"], w4["wup"], w4["wdown"], kc[l], vc[l]))
+    layers = ss.make_layers(descs)
+    gamma = gdev.normal_f16_device(seed, wl.FINAL_NORM_STREAM, (s.H,), 1.0, 0.02, dev)
+    lm_w = gdev.normal_f16_device(seed, wl.LM_HEAD_STREAM, (cfg.vocab, s.H), 0.0, 0.02, dev)
+    x = gdev.normal_f16_device(cfg.seeds()["activations"], 0, (T, s.H), device=dev)
+    parent, acc = wl.make_tree(cfg)
+    dparent = torch.from_numpy(np.asarray(parent, np.int32)).to(dev)
+    dacc = torch.tensor([acc], dtype=torch.int32, device=dev)
+    P_dev = torch.tensor([cfg.P], dtype=torch.int32, device=dev)
+    rope = torch.from_numpy(ss.rope_table(500000.0, cfg.S_max, s.D)).to(dev)
+    dims = ss.make_dims(s.H, s.Hq, s.Hkv, s.D, s.F, cfg.S_max)
+    ws = ss.workspace(ss.verify_step_workspace_bytes(dims, T, cfg.vocab), dev)
+    hidden = torch.empty_like(x)
+    logits = torch.zeros((T, cfg.vocab), dtype=torch.int16, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    def timed(enqueue, reps, warm=2):
+        g = ss.Graph()
+        with torch.cuda.stream(stream):
+            g.begin(stream)
+            enqueue()
+            g.end(stream)
+            for _ in range(warm):
+                g.launch(stream)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            ev[0].record(stream)
+            for i in range(reps):
+                g.launch(stream)
+                ev[i + 1].record(stream)
+        ev[-1].synchronize()
+        return sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(reps))
+
+    def step():
+        hidden.copy_(x)  # the tree tokens' embeddings enter the step
+        ss.verify_step(layers, dims, hidden, P_dev, dparent, rope, ws, gamma, lm_w, logits, stream=stream)
+
+    ms = timed(step, args.full_step_reps)
+    if ss.read_device_error(ws, stream):
+        raise RuntimeError("device error in the 80-layer step")
+    head_ms = timed(lambda: ss.lm_head(hidden, gamma, lm_w, logits, ws, stream=stream), args.full_step_reps)
+    commit_ms = timed(lambda: ss.kv_commit(kc, vc, P_dev, dparent, dacc, n_layers=nl, advance=False, ws=ws,
+                                           stream=stream), args.full_step_reps)
+    med = lambda v: v[len(v) // 2]
+    w_bytes = nl * s.w4_bytes()
+    kv_bytes = nl * cfg.kv_bytes_per_layer()
+    head_bytes = cfg.vocab * s.H * 2 + T * cfg.vocab * 2
+    step_bytes = w_bytes + kv_bytes + head_bytes
+    mean_ms = sum(ms) / len(ms)
+    out = {"workload": f"{cfg.name}: {nl} Llama-3-70B-shaped layers (int4 g128) + final RMSNorm + fp16 LM head "
+                       f"V={cfg.vocab}; tree T={T} ({cfg.levels} levels, branching<={cfg.branching}); "
+                       f"prefix P={cfg.P}; one HIP graph per step",
+           "ms_per_step": round(mean_ms, 4), "ms_p50": round(med(ms), 4),
+           "us_per_layer_incl_head": round(mean_ms * 1000.0 / nl, 2),
+           "algorithmic_bytes": step_bytes,
+           "hbm_gbs": round(step_bytes / (mean_ms * 1e-3) / 1e9, 1),
+           "frac_hbm": round(step_bytes / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "lm_head_us": round(med(head_ms) * 1000.0, 2),
+           "lm_head_gbs": round((head_bytes + T * s.H * 4) / (med(head_ms) * 1e-3) / 1e9, 1),
+           "kv_commit_all_layers_us": round(med(commit_ms) * 1000.0, 2),
+           "reps": args.full_step_reps, "setup_s": round(setup_s, 1),
+           "weights": "drawn on the device with the workload recipe (torch generator, seeded)"}
+    del keep, kc, vc, lm_w
+    torch.cuda.empty_cache()
+    return out
 
 
 def run_only(args, ss, torch, np, inst, cfg, dims, dparent, dacc, rope, stream, dev):

@@ -22,9 +22,10 @@
 // column) comes from the row-major tile through ds_read_b64_tr_b16: in each
 // 16-lane group, lane j receives element j % 4 of the 8-byte rows addressed
 // by lanes j / 4 + 4e, e = 0..3.  Online softmax in fp32, base 2.
-// The S + 1 partial results (unnormalised O, running max, running sum) of a
-// row block are merged by a second kernel on the same stream, in split
-// order, so results are deterministic.  blockIdx % Hkv = g keeps one head's
+// Each split publishes its rows' output normalised by their own softmax
+// sum (fp16) and their log-sum-exp (fp32); a second kernel on the same
+// stream merges the S + 1 partials of a row block in split order, so
+// results are deterministic.  blockIdx % Hkv = g keeps one head's
 // workgroups on one XCD when Hkv divides 8.
 #include "ss_device.h"
 #include "ss_internal.h"
@@ -55,13 +56,15 @@ struct AttnArgs {
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 // Bytes of one workgroup's partial: O normalised by its row sum, fp16
-// [W waves][D/16 d-tiles][64 lanes][4 rows], then fp32 (max, sum) of its
-// 16 W rows.  Normalised values are bounded by max |v|, so fp16 holds them
-// with the output's own precision.
+// [W waves][D/16 d-tiles][64 lanes][4 rows], then the fp32 base-2
+// log-sum-exp m + log2(l) of its 16 W rows (-inf for a row that saw no
+// key).  Normalised values are bounded by max |v|, so fp16 holds them with
+// the output's own precision.
 template <int D>
 __host__ __device__ constexpr size_t attn_part_bytes(int waves) {
-  return (size_t)waves * (D / 16) * kWave * 8 + (size_t)waves * 16 * 8;
+  return (size_t)waves * (D / 16) * kWave * 8 + (size_t)waves * 16 * 4;
 }
+constexpr int kMaxParts = 16;  // prefix splits + tree split, merged in one pass
 
 template <int D, int W>
 __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
@@ -90,7 +93,50 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
   const int rb = rest / (a.nsplit + 1);
   const bool tree_split = sp == a.nsplit;
 
-  // ---- per-step device data: prefix length and tree masks ----
+  // ---- prefix length; this split's first key tiles go out before anything
+  // else (an out-of-range P addresses from 0 and is rejected below) ----
+  const int P_dev = __builtin_amdgcn_readfirstlane(*a.prefix_len);
+  const bool p_ok = P_dev >= 0 && P_dev <= a.S_max - a.T;
+  const int P = p_ok ? P_dev : 0;
+  int k_lo = 0, k_hi = 0, ntiles = 0;
+  if (!tree_split) {
+    const int per = (P + a.nsplit - 1) / a.nsplit;
+    const int chunk = ((per + kKeyTile - 1) / kKeyTile) * kKeyTile;
+    k_lo = min(P, sp * chunk);
+    k_hi = min(P, k_lo + chunk);
+    ntiles = (k_hi - k_lo + kKeyTile - 1) / kKeyTile;
+  }
+  k_lo = __builtin_amdgcn_readfirstlane(k_lo);
+  k_hi = __builtin_amdgcn_readfirstlane(k_hi);
+  ntiles = __builtin_amdgcn_readfirstlane(ntiles);
+  const uint16_t* kc = a.k_cache + (size_t)g * a.S_max * D;
+  const uint16_t* vc = a.v_cache + (size_t)g * a.S_max * D;
+  u32x4 kbuf[kAttnRing][NV], vbuf[kAttnRing][NV];
+  // tile t (clamped to the chunk's last; rows past k_hi repeat row k_hi - 1
+  // and are masked).  Only called when ntiles > 0.
+  auto load_tile = [&](int t, u32x4 (&kd)[NV], u32x4 (&vd)[NV]) {
+    int tt = __builtin_amdgcn_readfirstlane(t < ntiles ? t : ntiles - 1);
+    asm volatile("" : "+s"(tt));
+    const int key0 = k_lo + tt * kKeyTile;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int idx = tid + j * NT;
+      const int key = min(key0 + idx / VPR, k_hi - 1);
+      const int c8 = (idx % VPR) * 8;
+      kd[j] = *reinterpret_cast<const u32x4*>(kc + (size_t)key * D + c8);
+      vd[j] = *reinterpret_cast<const u32x4*>(vc + (size_t)key * D + c8);
+    }
+  };
+  auto retire = [&](const u32x4 (&kd)[NV], const u32x4 (&vd)[NV]) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) asm volatile("" : : "v"(kd[j]), "v"(vd[j]));
+  };
+  if (ntiles > 0) {
+#pragma unroll
+    for (int j = 0; j < kAttnRing - 1; ++j) load_tile(j, kbuf[j], vbuf[j]);
+  }
+
+  // ---- tree masks and validity ----
   if (wave == 0) {
     uint64_t anc;
     int depth;
@@ -98,10 +144,9 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
     s_anc[lane] = anc;
     s_depth[lane] = depth;
     if (lane == 0) {
-      const int P = *a.prefix_len;
       int st = 0;
       if (!ok) st |= SWIFTSPEC_DEVERR_BAD_TREE;
-      if (P < 0 || P > a.S_max - a.T) st |= SWIFTSPEC_DEVERR_BAD_PREFIX;
+      if (!p_ok) st |= SWIFTSPEC_DEVERR_BAD_PREFIX;
       s_status = st;
       if (st && blockIdx.x == 0) report_error(a.ws, (uint32_t)st);
     }
@@ -110,13 +155,16 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
   const int nparts = a.nsplit + 1;
   const size_t grp = (size_t)g * a.RB + rb;
   char* mine = reinterpret_cast<char*>(a.part) + (grp * nparts + sp) * attn_part_bytes<D>(W);
-  float* ml = reinterpret_cast<float*>(mine + (size_t)W * (D / 16) * kWave * 8);
+  float* lse = reinterpret_cast<float*>(mine + (size_t)W * (D / 16) * kWave * 8);
   if (s_status) {
     // invalid tree or prefix: empty partials, so the merge leaves the output alone
-    if (tid < 16 * W) *reinterpret_cast<f32x2*>(ml + tid * 2) = f32x2{-INFINITY, 0.f};
+    if (ntiles > 0) {
+#pragma unroll
+      for (int j = 0; j < kAttnRing - 1; ++j) retire(kbuf[j], vbuf[j]);
+    }
+    if (tid < 16 * W) lse[tid] = -INFINITY;
     return;
   }
-  const int P = *a.prefix_len;
 
   // ---- this wave's 16 query rows: rotated Q as B fragments ----
   const int row = rb * (16 * W) + wave * 16 + n16;
@@ -277,31 +325,8 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
     __syncthreads();
     compute(0, a.T, true);
   } else {
-    // ---- prefix chunk of this split ----
-    const int per = (P + a.nsplit - 1) / a.nsplit;
-    const int chunk = ((per + kKeyTile - 1) / kKeyTile) * kKeyTile;
-    const int k_lo = min(P, sp * chunk);
-    const int k_hi = min(P, k_lo + chunk);
-    const int ntiles = (k_hi - k_lo + kKeyTile - 1) / kKeyTile;
+    // ---- prefix chunk of this split (first tiles already in flight) ----
     if (ntiles > 0) {
-      const uint16_t* kc = a.k_cache + (size_t)g * a.S_max * D;
-      const uint16_t* vc = a.v_cache + (size_t)g * a.S_max * D;
-      u32x4 kr[kAttnRing][NV], vr[kAttnRing][NV];
-      // tile t (clamped to the chunk's last; rows past k_hi repeat row
-      // k_hi - 1 and are masked)
-      auto load_tile = [&](int t, u32x4 (&kd)[NV], u32x4 (&vd)[NV]) {
-        int tt = t < ntiles ? t : ntiles - 1;
-        asm volatile("" : "+s"(tt));
-        const int key0 = k_lo + tt * kKeyTile;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-          const int idx = tid + j * NT;
-          const int key = min(key0 + idx / VPR, k_hi - 1);
-          const int c8 = (idx % VPR) * 8;
-          kd[j] = *reinterpret_cast<const u32x4*>(kc + (size_t)key * D + c8);
-          vd[j] = *reinterpret_cast<const u32x4*>(vc + (size_t)key * D + c8);
-        }
-      };
       auto store_tile = [&](int slot, const u32x4 (&kd)[NV], const u32x4 (&vd)[NV]) {
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
@@ -311,9 +336,7 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
           *reinterpret_cast<u32x4*>(&vs[slot][off]) = vd[j];
         }
       };
-#pragma unroll
-      for (int j = 0; j < kAttnRing - 1; ++j) load_tile(j, kr[j], vr[j]);
-      store_tile(0, kr[0], vr[0]);
+      store_tile(0, kbuf[0], vbuf[0]);
       // step t: load tile t + 4, write tile t + 1 to LDS slot (t + 1) % 3
       // (last read at step t - 2), barrier, compute tile t; whole rounds of
       // five steps, steps past the end only load (the first one leaves)
@@ -321,14 +344,13 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
         for (int J = 0; J < kAttnRing; ++J) {
           const int t = t0 + J;
-          load_tile(t + kAttnRing - 1, kr[(J + kAttnRing - 1) % kAttnRing], vr[(J + kAttnRing - 1) % kAttnRing]);
+          load_tile(t + kAttnRing - 1, kbuf[(J + kAttnRing - 1) % kAttnRing], vbuf[(J + kAttnRing - 1) % kAttnRing]);
           if (t < ntiles) {
-            if (t + 1 < ntiles) store_tile((t + 1) % kAttnLds, kr[(J + 1) % kAttnRing], vr[(J + 1) % kAttnRing]);
+            if (t + 1 < ntiles) store_tile((t + 1) % kAttnLds, kbuf[(J + 1) % kAttnRing], vbuf[(J + 1) % kAttnRing]);
             lds_barrier();
             compute(t % kAttnLds, k_hi - (k_lo + t * kKeyTile), false);
           } else {
-#pragma unroll
-            for (int j = 0; j < NV; ++j) asm volatile("" : : "v"(kr[J][j]), "v"(vr[J][j]));
+            retire(kbuf[J], vbuf[J]);
           }
         }
       }
@@ -348,21 +370,20 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
     const uint32_t hi = (uint32_t)f2h(o[dt][2] * inv[2]) | ((uint32_t)f2h(o[dt][3] * inv[3]) << 16);
     *reinterpret_cast<u32x2*>(mine + ((size_t)(wave * DT + dt) * kWave + lane) * 8) = u32x2{lo, hi};
   }
-  if (kq == 0) *reinterpret_cast<f32x2*>(ml + (wave * 16 + n16) * 2) = f32x2{m_run, l_run};
+  if (kq == 0) lse[wave * 16 + n16] = l_run > 0.f ? m_run + __log2f(l_run) : -INFINITY;
 }
 
-// Merge of the S + 1 partials of one 16-row x 16-column output tile in
-// split order: running (max, sum) and O (partial rows times their sums)
-// rescaled to the running max.  All loads of up to 16 splits are issued
-// together (the kernel is a few memory round trips long).  Grid = Hkv x RB
-// x W x D/16, one wave each (lane: rows 4 (lane / 16) + r, column
-// lane % 16).  A row with no key at all (only possible when the attention
-// kernel rejected the tree or the prefix and published empty partials) is
-// not written.
+// Merge of the S + 1 <= 16 partials of one 16-row x 16-column output tile,
+// in split order: with L_s the log-sum-exp of a row in split s and O_s its
+// normalised output, O = sum_s 2^(L_s - L) O_s, L = log2 sum_s 2^L_s (taken
+// relative to max_s L_s).  One wave per tile (lane: rows 4 (lane / 16) + r,
+// column lane % 16); every split's loads are issued at once, so the kernel
+// is one memory round trip long.  Grid = Hkv x RB x W x D/16.  A row that no
+// split saw (only when the attention kernel rejected the tree or the prefix
+// and published empty partials) is not written.
 template <int D, int W>
 __global__ __launch_bounds__(64) void tree_attention_merge_kernel(AttnArgs a) {
   constexpr int DT = D / 16;
-  constexpr int kBatch = 16;
   const int lane = lane_id();
   const int n16 = lane & 15, kq = lane >> 4;
   const int dt = blockIdx.x % DT;
@@ -372,45 +393,35 @@ __global__ __launch_bounds__(64) void tree_attention_merge_kernel(AttnArgs a) {
   const int nparts = a.nsplit + 1;
   const size_t part_stride = attn_part_bytes<D>(W);
   const char* base = reinterpret_cast<const char*>(a.part) + (size_t)grp * nparts * part_stride;
-  float mrun[4], lrun[4];
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4 ls[kMaxParts];
+  u32x2 ov[kMaxParts];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) mrun[r] = -INFINITY, lrun[r] = 0.f;
-  for (int s0 = 0; s0 < nparts; s0 += kBatch) {
-    f32x2 mlr[kBatch];  // (max, sum) of row n16 of this wave
-    u32x2 ov[kBatch];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int s2 = s0 + j < nparts ? s0 + j : nparts - 1;
-      const char* src = base + s2 * part_stride;
-      const float* mlp = reinterpret_cast<const float*>(src + (size_t)W * DT * kWave * 8);
-      mlr[j] = *reinterpret_cast<const f32x2*>(mlp + (wave * 16 + n16) * 2);
-      ov[j] = *reinterpret_cast<const u32x2*>(src + ((size_t)(wave * DT + dt) * kWave + lane) * 8);
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      if (s0 + j >= nparts) break;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float mp = __shfl(mlr[j][0], 4 * kq + r, kWave);
-        const float lp0 = __shfl(mlr[j][1], 4 * kq + r, kWave);
-        const float m_new = fmaxf(mrun[r], mp);
-        const float w_old = (mrun[r] == -INFINITY) ? 0.f : exp2f(mrun[r] - m_new);
-        const float w_new = (mp == -INFINITY) ? 0.f : exp2f(mp - m_new);
-        const float lp = lp0 * w_new;
-        const float on = h2f((uint16_t)(ov[j][r >> 1] >> (16 * (r & 1))));
-        lrun[r] = lrun[r] * w_old + lp;
-        acc[r] = acc[r] * w_old + on * lp;
-        mrun[r] = m_new;
-      }
-    }
+  for (int j = 0; j < kMaxParts; ++j) {
+    const char* src = base + (size_t)(j < nparts ? j : nparts - 1) * part_stride;
+    ls[j] = *reinterpret_cast<const f32x4*>(src + (size_t)W * DT * kWave * 8 + (wave * 16 + 4 * kq) * 4);
+    ov[j] = *reinterpret_cast<const u32x2*>(src + ((size_t)(wave * DT + dt) * kWave + lane) * 8);
   }
+  float lmax[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+  for (int j = 0; j < kMaxParts; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (j < nparts) lmax[r] = fmaxf(lmax[r], ls[j][r]);
+  float wsum[4] = {0.f, 0.f, 0.f, 0.f}, acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < kMaxParts; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float w = (j < nparts && ls[j][r] != -INFINITY) ? exp2f(ls[j][r] - lmax[r]) : 0.f;
+      wsum[r] += w;
+      acc[r] += w * h2f((uint16_t)(ov[j][r >> 1] >> (16 * (r & 1))));
+    }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int orow = rb * (16 * W) + wave * 16 + 4 * kq + r;
-    if (orow < a.R && lrun[r] > 0.f) {
+    if (orow < a.R && lmax[r] != -INFINITY) {
       const int i = orow / a.G, qh = g * a.G + orow % a.G;
-      const uint16_t h = f2h(acc[r] / lrun[r]);
+      const uint16_t h = f2h(acc[r] / wsum[r]);
       a.out[(size_t)i * a.ldo + qh * D + dt * 16 + n16] = h;
       if (a.out_prep) store_prepared(a.out_prep, i, qh * D + dt * 16 + n16, (a.Hq * D) >> 7, h);
     }
@@ -430,6 +441,7 @@ AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max) {
   int ns = 256 / groups - 1;
   const int max_tiles = (S_max - T + kKeyTile - 1) / kKeyTile;
   if (ns > max_tiles / 4) ns = max_tiles / 4;
+  if (ns > kMaxParts - 1) ns = kMaxParts - 1;
   if (ns < 1) ns = 1;
   p.nsplit = ns;
   p.chunk = 0;

@@ -12,16 +12,14 @@
 //   * Lane (n = lane % 16, kq = lane / 16) loads 16 bytes = k in
 //     [128 g + 32 kq, +32) of weight row n: one wave-wide load covers one
 //     16-column x 128-k block, i.e. exactly one (scale, zero) group.
-//   * Dequantisation by masking only: (w & 0x000F000F) is the fp16 pair
-//     (q * 2^-24, q' * 2^-24) (subnormals, which the matrix cores take
-//     exactly) and (w & 0x00F000F0) is (16 q * 2^-24, ...).  Low-nibble slots
+//   * Dequantisation to exact integers with the fp16 "magic number" 1024:
+//     OR-ing a nibble field into 0x6400 gives 1024 + q (low nibble) or
+//     1024 + 16 q (high nibble), and one packed fp16 subtraction of 1024 + z
+//     (1024 + 16 z) leaves q - z (16 (q - z)) exactly.  Low-nibble slots
 //     meet activations pre-multiplied by 16, so every product is
-//     x * q * 2^-20 exactly and the MFMA sum of a group is
-//     C_g = 2^-20 sum_k x q.  The zero point is applied through the row sums
-//     S_g[m] = sum_k x[m][k] of the group (four more MFMAs per M-tile
-//     against constant B fragments, landing directly in the accumulator
-//     layout; every wave forms them from the fragments it reads anyway):
-//         y += s * 2^20 * C_g - (s * z) * S_g.
+//     16 x (q - z) exactly and the MFMA sum of a group is
+//     C_g = 16 sum_k x (q - z); per group y += (s / 16) C_g (one FMA per
+//     output element).
 //   * Stream-K scheduling: a fixed grid of workgroups (4 waves each) splits
 //     the (N-block, group) iteration space into equal contiguous ranges; the
 //     4 waves split an N-block's columns.  Per group, every wave loads 1 KB
@@ -78,15 +76,18 @@ struct BStage {
 
 // Kernel shapes.  R = register-ring depth (groups whose loads are in flight
 // or waiting to be used), OCC = waves per SIMD the register budget is cut
-// for.  Measured on the Llama-3-70B layer: a shallow ring with three waves
-// per SIMD (768 workgroups) suits the long SwiGLU stream, four groups at two
-// waves per SIMD (512 workgroups) the shorter projections; above 32 rows the
-// accumulators take the registers (one workgroup per CU).
+// for, NWG = workgroup cap.  Measured on the Llama-3-70B layer: the SwiGLU
+// stream runs a shallow ring at three waves per SIMD, one workgroup per
+// N-block when there are enough N-blocks to fill the chip (no split, so no
+// partials and no fix-up kernel); the shorter projections four groups deep
+// at two waves per SIMD over 512 workgroups (fewer, deeper-ringed
+// workgroups were slower); above 32 rows the accumulators take the
+// registers (one workgroup per CU).
 struct GemmShape {
   int ring, occ, nwg;
 };
 constexpr GemmShape gemm_shape(int MT, bool swiglu) {
-  return MT > 2 ? GemmShape{4, 1, 256} : swiglu ? GemmShape{3, 3, 768} : GemmShape{4, 2, 512};
+  return MT > 2 ? GemmShape{4, 1, 256} : swiglu ? GemmShape{3, 2, 768} : GemmShape{3, 2, 512};
 }
 constexpr int kRingL = 3;  // LDS ring of activation fragments
 
@@ -227,50 +228,61 @@ void w4a16_gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Row sums of the group's activations in accumulator layout: MFMA against
-  // constant B fragments (1/16 for the x16-scaled low-nibble slots, 1 else);
-  // every wave forms them from the fragments it has already read.
-  const half8 one16 = {(_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f,
-                       (_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f, (_Float16)0.0625f};
-  const half8 one = {(_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f,
-                     (_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f};
-  auto compute = [&](int slot, const BStage<MT, NWV>& st) {
-    half8 af[MT][4];
-    f32x4 sx[MT];
+  // Dequantisation to exact small integers: (w & 0x000F000F) | 0x64006400
+  // is the fp16 pair (1024 + q, 1024 + q'), (w & 0x00F000F0) | 0x64006400 is
+  // (1024 + 16 q, ...); subtracting 1024 + z (resp. 1024 + 16 z) leaves
+  // q - z (resp. 16 (q - z)) exactly.  Low-nibble slots meet activations
+  // pre-multiplied by 16, so the MFMA sum of a group is C_g = 16 sum_k x (q - z)
+  // and y += (s / 16) C_g.
+  // The magic constant is kept in a register (opaque to the optimiser) so
+  // that mask-and-insert is one v_bfi_b32 with the mask in a scalar register.
+  uint32_t magic = 0x64006400u;
+  asm volatile("" : "+v"(magic));
+  auto deq = [&](uint32_t x, uint32_t m, half2v zz) {
+    return bitcast<uint32_t>(bitcast<half2v>((x & m) | (magic & ~m)) - zz);
+  };
+  auto read_a = [&](int slot, half8 (&af)[MT][4]) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int f = 0; f < 4; ++f) af[mt][f] = bitcast<half8>(abuf[slot][mt][f][lane]);
-      f32x4 c = {0.f, 0.f, 0.f, 0.f};
-      c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][0], one16, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][1], one16, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][2], one, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][3], one, c, 0, 0, 0);
-      sx[mt] = c;
-    }
+  };
+  // group sums C_g of one unit (and the tiles' s / 16); applied to the
+  // accumulators one step later, so that no instruction waits on the MFMAs
+  // just issued
+  auto mfma_unit = [&](const half8 (&af)[MT][4], const BStage<MT, NWV>& st, f32x4 (&c)[MT][NWV],
+                       float (&s16)[NWV]) {
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
       const u32x4 w = st.b[nt];
       const uint32_t s0 = w[0] >> 8, s1 = w[1] >> 8, s2 = w[2] >> 8, s3 = w[3] >> 8;
-      const half8 blo_a = bitcast<half8>(u32x4{w[0] & 0x000F000Fu, s0 & 0x000F000Fu, w[1] & 0x000F000Fu, s1 & 0x000F000Fu});
-      const half8 blo_b = bitcast<half8>(u32x4{w[2] & 0x000F000Fu, s2 & 0x000F000Fu, w[3] & 0x000F000Fu, s3 & 0x000F000Fu});
-      const half8 bhi_a = bitcast<half8>(u32x4{w[0] & 0x00F000F0u, s0 & 0x00F000F0u, w[1] & 0x00F000F0u, s1 & 0x00F000F0u});
-      const half8 bhi_b = bitcast<half8>(u32x4{w[2] & 0x00F000F0u, s2 & 0x00F000F0u, w[3] & 0x00F000F0u, s3 & 0x00F000F0u});
-      const float sc = h2f((uint16_t)(st.sz[nt] & 0xFFFFu));
-      const float s20 = sc * 1048576.0f;
-      const float nsz = -sc * (float)((st.sz[nt] >> 16) & 0xFFu);
+      constexpr uint32_t kLo = 0x000F000Fu, kHi = 0x00F000F0u;
+      const uint32_t z = (st.sz[nt] >> 16) & 0xFFu;
+      const half2v zlo = bitcast<half2v>((0x6400u + z) * 0x00010001u);
+      const half2v zhi = bitcast<half2v>((0x6400u + 16u * z) * 0x00010001u);
+      const half8 blo_a = bitcast<half8>(u32x4{deq(w[0], kLo, zlo), deq(s0, kLo, zlo), deq(w[1], kLo, zlo), deq(s1, kLo, zlo)});
+      const half8 blo_b = bitcast<half8>(u32x4{deq(w[2], kLo, zlo), deq(s2, kLo, zlo), deq(w[3], kLo, zlo), deq(s3, kLo, zlo)});
+      const half8 bhi_a = bitcast<half8>(u32x4{deq(w[0], kHi, zhi), deq(s0, kHi, zhi), deq(w[1], kHi, zhi), deq(s1, kHi, zhi)});
+      const half8 bhi_b = bitcast<half8>(u32x4{deq(w[2], kHi, zhi), deq(s2, kHi, zhi), deq(w[3], kHi, zhi), deq(s3, kHi, zhi)});
+      s16[nt] = h2f((uint16_t)(st.sz[nt] & 0xFFFFu)) * 0.0625f;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        f32x4 c = {0.f, 0.f, 0.f, 0.f};
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][0], blo_a, c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][1], blo_b, c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][2], bhi_a, c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][3], bhi_b, c, 0, 0, 0);
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          acc[mt][nt][r] = __builtin_fmaf(sx[mt][r], nsz, __builtin_fmaf(c[r], s20, acc[mt][nt][r]));
+        f32x4 cc = {0.f, 0.f, 0.f, 0.f};
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][0], blo_a, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][1], blo_b, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][2], bhi_a, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][3], bhi_b, cc, 0, 0, 0);
+        c[mt][nt] = cc;
       }
     }
+  };
+  auto apply = [&](const f32x4 (&c)[MT][NWV], const float (&s16)[NWV]) {
+#pragma unroll
+    for (int nt = 0; nt < NWV; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[mt][nt][r] = __builtin_fmaf(c[mt][nt][r], s16[nt], acc[mt][nt][r]);
   };
 
   auto emit = [&](int nb) {
@@ -339,26 +351,50 @@ void w4a16_gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) asm volatile("" : : "v"(r[mt]));
   };
+  // Activation fragments and group sums are double-buffered: at step i the
+  // wave reads unit i + 1's fragments (its LDS slot is complete once the
+  // barrier of step i has passed) and applies unit i - 1's sums.
+  half8 af[2][MT][4];
+  f32x4 cs[2][MT][NWV];
+  float sc[2][NWV];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int nt = 0; nt < NWV; ++nt) {
+      sc[q][nt] = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) cs[q][mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  lds_barrier();
+  read_a(0, af[0]);
   // compute cursor: N-block and group of unit i
   int c_nb = u_lo / G, c_g = u_lo - (u_lo / G) * G;
-  for (int i0 = 0; i0 < total; i0 += kRing) {
+  for (int i0 = 0; i0 < total; i0 += 2 * kRing) {
 #pragma unroll
-    for (int J = 0; J < kRing; ++J) {
+    for (int J = 0; J < 2 * kRing; ++J) {
       const int i = i0 + J;
-      load_a(ar[(J + kRing - 1) % kRing]);
-      load_b(bs[(J + kRing - 1) % kRing]);
+      const int R = J % kRing, bq = J & 1;
+      load_a(ar[(R + kRing - 1) % kRing]);
+      load_b(bs[(R + kRing - 1) % kRing]);
       advance();
       if (i < total) {
-        if (i + 1 < total) store_a((i + 1) % kRingL, ar[(J + 1) % kRing]);
+        if (i + 1 < total) store_a((i + 1) % kRingL, ar[(R + 1) % kRing]);
         lds_barrier();
-        compute(i % kRingL, bs[J]);
-        if (i == total - 1 || c_g == G - 1) flush(c_nb);
+        if (i + 1 < total) read_a((i + 1) % kRingL, af[bq ^ 1]);
+        mfma_unit(af[bq], bs[R], cs[bq], sc[bq]);
+        apply(cs[bq ^ 1], sc[bq ^ 1]);
+        if (i == total - 1 || c_g == G - 1) {
+          apply(cs[bq], sc[bq]);
+#pragma unroll
+          for (int nt = 0; nt < NWV; ++nt) sc[bq][nt] = 0.f;
+          flush(c_nb);
+        }
         if (++c_g == G) {
           c_g = 0;
           ++c_nb;
         }
       } else {
-        consume(bs[J], ar[(J + 1) % kRing]);
+        consume(bs[R], ar[(R + 1) % kRing]);
       }
     }
   }
@@ -562,7 +598,9 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
     p.nblocks = tiles / (4 * p.nw);
   }
   const long units = (long)p.nblocks * (K / 128);
-  const int cap = gemm_shape(MT, swiglu).nwg;
+  int cap = gemm_shape(MT, swiglu).nwg;
+  // whole N-blocks per workgroup when they alone fill the chip
+  if (swiglu && MT <= 2 && p.nblocks >= 256 && p.nblocks <= 2 * cap) cap = p.nblocks;
   p.nwg = (int)(units < cap ? units : cap);
   const int col_w = swiglu ? p.nw / 2 : p.nw;
   const int src = swiglu ? 2 : 1;

@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-full-step", action="store_true",
                     help="skip the 80-layer step (all layers + final norm + LM head) timing")
     ap.add_argument("--full-step-reps", type=int, default=10)
+    ap.add_argument("--gemm-ab", action="store_true",
+                    help="only compare the matrix-core and vector-ALU W4A16 GEMMs over M (JSON line per M)")
     return ap.parse_args()
 
 
@@ -137,6 +139,10 @@ def main():
         d["ws"] = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
         inst.append(d)
     torch.cuda.synchronize()
+
+    if args.gemm_ab:
+        gemm_ab(ss, torch, np, inst, cfg, stream, dev)
+        return
 
     # ---------------- counter-run mode: one kernel type only ----------------
     if args.only_kernel:
@@ -400,6 +406,49 @@ def full_step(args, ss, torch, np, dev, stream):
     del keep, kc, vc, lm_w
     torch.cuda.empty_cache()
     return out
+
+
+def gemm_ab(ss, torch, np, inst, cfg, stream, dev):
+    """Matrix-core against vector-ALU W4A16 GEMM: the layer's four weight
+    shapes (gate alone for the SwiGLU width) at M = 1 .. 64, each entry point
+    called on rotated weight copies inside a replayed graph; one JSON line
+    per M with microseconds, algorithmic GB/s and the VALU / MFMA time ratio."""
+    s = cfg.shape
+    copies = len(inst)
+    shapes = [("qkv", "wqkv", s.H, s.n_qkv), ("o_proj", "wo", s.Hq * s.D, s.H), ("gate", "wgate", s.H, s.F),
+              ("down", "wdown", s.F, s.H)]
+    w4b = lambda K, N: K * N // 2 + (K // 128) * N * 3
+    for M in (1, 2, 4, 8, 16, 32, 64):
+        x = (torch.randn((M, max(s.H, s.F)), device=dev) * 1.0).half().view(torch.int16)
+        y = torch.zeros((M, max(s.F, s.n_qkv)), dtype=torch.int16, device=dev)
+        out = {"gemm_ab_M": M}
+        for name, wname, K, N in shapes:
+            ws_m = ss.workspace(ss.gemm_workspace_bytes(M, K, N), dev)
+            ws_v = ss.workspace(ss.gemm_valu_workspace_bytes(M, K, N), dev)
+            res = {}
+            for kind, fn in (("mfma", lambda d: ss.w4a16_gemm(d, x[:, :K], y[:, :N], ws_m, stream=stream)),
+                             ("valu", lambda d: ss.w4a16_gemm_valu(d, x[:, :K], y[:, :N], ws_v, stream=stream))):
+                g = ss.Graph()
+                iters = 30
+                with torch.cuda.stream(stream):
+                    for i in range(3):
+                        fn(inst[i % copies]["w4"][wname])
+                    g.begin(stream)
+                    for i in range(iters):
+                        fn(inst[i % copies]["w4"][wname])
+                    g.end(stream)
+                    g.launch(stream)
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    for _ in range(3):
+                        g.launch(stream)
+                    e1.record(stream)
+                e1.synchronize()
+                us = e0.elapsed_time(e1) * 1000.0 / (3 * iters)
+                res[kind] = {"us": round(us, 2), "GBps": round(w4b(K, N) / (us * 1e-6) / 1e9, 1)}
+            res["valu_over_mfma"] = round(res["valu"]["us"] / res["mfma"]["us"], 2)
+            out[name] = res
+        print(json.dumps(out), flush=True)
 
 
 def run_only(args, ss, torch, np, inst, cfg, dims, dparent, dacc, rope, stream, dev):

@@ -131,6 +131,17 @@ int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const
                            size_t ws_bytes, void* stream);
 size_t swiftspec_w4a16_swiglu_workspace_bytes(int32_t M, int32_t K, int32_t N);
 
+/* The same product as swiftspec_w4a16_gemm computed on the vector ALUs
+ * only (v_dot2_f32_f16, no matrix cores): the comparison point for the
+ * matrix-core kernel at M = tree size (Sec. 3.3, Sec. 5.1).  Same arguments,
+ * constraints and result tolerance; fp32 partial sums per K slice are added
+ * in slice order (deterministic).  Workspace from
+ * swiftspec_w4a16_gemm_valu_workspace_bytes. */
+int swiftspec_w4a16_gemm_valu(const swiftspec_w4* W, const uint16_t* x, int32_t M, int32_t ldx,
+                              uint16_t* y, int32_t ldy, const uint16_t* residual, int32_t ldr,
+                              void* ws, size_t ws_bytes, void* stream);
+size_t swiftspec_w4a16_gemm_valu_workspace_bytes(int32_t M, int32_t K, int32_t N);
+
 /* Activations in the matrix-core operand order the GEMMs read
  * ("prepared" layout: [ceil(M/16)][K/128][4][64][8] fp16, rows >= M zero,
  * even k of every 32-wide slice stored times 16).  Chained GEMMs can keep

@@ -88,6 +88,8 @@ _SIGS = {
     "swiftspec_verify_step": ([ctypes.POINTER(Layer), i32, ctypes.POINTER(Dims), vp, i32, vp, vp, vp, vp, vp,
                                i32, vp, vp, sz, vp], ctypes.c_int),
     "swiftspec_verify_step_workspace_bytes": ([ctypes.POINTER(Dims), i32, i32], sz),
+    "swiftspec_w4a16_gemm_valu": ([ctypes.POINTER(W4), vp, i32, i32, vp, i32, vp, i32, vp, sz, vp], ctypes.c_int),
+    "swiftspec_w4a16_gemm_valu_workspace_bytes": ([i32, i32, i32], sz),
     "swiftspec_graph_begin": ([vp], ctypes.c_int),
     "swiftspec_graph_end": ([vp, ctypes.POINTER(vp)], ctypes.c_int),
     "swiftspec_graph_launch": ([vp, vp], ctypes.c_int),
@@ -194,6 +196,18 @@ def workspace_init(ws, stream=None):
 
 def gemm_workspace_bytes(M: int, K: int, N: int) -> int:
     return int(_load().swiftspec_w4a16_gemm_workspace_bytes(M, K, N))
+
+
+def gemm_valu_workspace_bytes(M: int, K: int, N: int) -> int:
+    return int(_load().swiftspec_w4a16_gemm_valu_workspace_bytes(M, K, N))
+
+
+def w4a16_gemm_valu(W: W4, x, y, ws, residual=None, stream=None):
+    """As w4a16_gemm, on the vector ALUs only (comparison variant)."""
+    st = _load().swiftspec_w4a16_gemm_valu(ctypes.byref(W), _ptr(x), x.shape[0], x.stride(0), _ptr(y), y.stride(0),
+                                           _ptr(residual), residual.stride(0) if residual is not None else 0,
+                                           _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "w4a16_gemm_valu")
 
 
 def swiglu_workspace_bytes(M: int, K: int, N: int) -> int:

@@ -38,19 +38,17 @@ void launch_prepack_w4(const uint8_t* q, const uint16_t* s, const uint8_t* z, in
                        hipStream_t st);
 inline size_t w4_packed_bytes(int K, int N) { return (size_t)K * N / 2 + (size_t)N * (K / 128) * 4; }
 
-struct DenseGemmLaunch {
-  const uint16_t* w;  // [N][K] fp16
-  int K, N;
-  const uint16_t* x;
-  int M, ldx;
-  uint16_t* y;
-  int ldy;
-  int nw, nblocks, nsplit;
-  float* part;
-  uint32_t* counters;
+// VALU dot-product variant of the W4A16 GEMM (no matrix cores): one wave
+// per (16-column tile, K slice), fp32 partial sums per slice, summed in
+// slice order by a second kernel that also adds the residual.
+struct ValuGemmPlan {
+  int ksplit, gslice;  // K slices and groups per slice
+  size_t part_bytes;   // [ksplit][M][N] fp32
 };
-GemmPlan plan_dense_gemm(int M, int K, int N);
-void launch_dense_gemm(const DenseGemmLaunch& L, hipStream_t st);
+ValuGemmPlan plan_w4a16_gemm_valu(int M, int K, int N);
+void launch_w4a16_gemm_valu(const void* packed, int K, int N, const uint16_t* aprep, int M, uint16_t* y,
+                            int ldy, const uint16_t* res, int ldr, float* part, const ValuGemmPlan& p,
+                            hipStream_t st);
 
 struct AttnLaunch {
   const uint16_t* q;

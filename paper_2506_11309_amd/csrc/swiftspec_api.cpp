@@ -269,6 +269,36 @@ int swiftspec_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, in
   return check_launch();
 }
 
+size_t swiftspec_w4a16_gemm_valu_workspace_bytes(int32_t M, int32_t K, int32_t N) {
+  if (M < 1 || K < 128 || N < 64) return kHeader;
+  const ss::GemmPlan g = ss::plan_w4a16_gemm(M, K, N, false);
+  const ss::ValuGemmPlan p = ss::plan_w4a16_gemm_valu(M, K, N);
+  return kHeader + align_up(g.prep_bytes) + align_up(p.part_bytes);
+}
+
+int swiftspec_w4a16_gemm_valu(const swiftspec_w4* W, const uint16_t* x, int32_t M, int32_t ldx, uint16_t* y,
+                              int32_t ldy, const uint16_t* residual, int32_t ldr, void* ws, size_t ws_bytes,
+                              void* stream) {
+  int rc = check_w4(W);
+  if (rc) return rc;
+  if (!x || !y || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (M < 0 || ldx < W->K || ldy < W->N || (residual && ldr < W->N)) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(x) || ldx % 8 || !aligned16(ws)) return SWIFTSPEC_MISALIGNED;
+  if (residual == y && ldr != ldy) return SWIFTSPEC_INVALID_ARG;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (ws_bytes < swiftspec_w4a16_gemm_valu_workspace_bytes(M, W->K, W->N)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  const ss::GemmPlan g = ss::plan_w4a16_gemm(M, W->K, W->N, false);
+  const ss::ValuGemmPlan p = ss::plan_w4a16_gemm_valu(M, W->K, W->N);
+  char* base = static_cast<char*>(ws);
+  uint16_t* aprep = reinterpret_cast<uint16_t*>(base + kHeader);
+  float* part = reinterpret_cast<float*>(base + kHeader + align_up(g.prep_bytes));
+  hipStream_t st = S(stream);
+  ss::launch_prepare_activations(x, M, ldx, W->K, aprep, st);
+  ss::launch_w4a16_gemm_valu(W->packed, W->K, W->N, aprep, M, y, ldy, residual, ldr, part, p, st);
+  return check_launch();
+}
+
 int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* x,
                            int32_t M, int32_t ldx, uint16_t* y, int32_t ldy, void* ws,
                            size_t ws_bytes, void* stream) {

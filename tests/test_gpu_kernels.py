@@ -236,6 +236,27 @@ def test_w4a16_swiglu_config_shapes(name):
     check_close(down16(dy), oracle.w4a16_swiglu(Wg, Wu, x), f"swiglu {name}")
 
 
+@pytest.mark.parametrize("M,K,N", [(1, 1024, 1024), (8, 2048, 512), (13, 1024, 2048), (32, 8192, 1024),
+                                   (40, 4096, 1024), (64, 2048, 1024)])
+def test_w4a16_gemm_valu_variant_matches_oracle(M, K, N):
+    """The vector-ALU comparison variant computes the same product (with a
+    residual) within the tolerance, deterministically."""
+    W = _rand_w4(21 + M, N, K)
+    x = gen.normal_f16(21, M, (M, K))
+    res = gen.normal_f16(22, M, (M, N))
+    t, d = upload_w4(W)
+    outs = []
+    for _ in range(2):
+        dy = torch.zeros((M, N), dtype=torch.int16, device=dev())
+        ws = ss.workspace(ss.gemm_valu_workspace_bytes(M, K, N), dev())
+        ss.w4a16_gemm_valu(d, up(x), dy, ws, residual=up(res))
+        torch.cuda.synchronize()
+        outs.append(down16(dy))
+    assert np.array_equal(outs[0], outs[1])
+    err, rel = check_close(outs[0], oracle.w4a16_gemm(W, x, residual=res), f"valu gemm M={M} K={K} N={N}")
+    print(f"valu gemm M={M} K={K} N={N}: max abs err {err:.3g}, rel {rel:.3g}")
+
+
 def test_w4a16_gemm_rejects_bad_arguments():
     W = _rand_w4(1, 64, 256)
     t, d = upload_w4(W)

@@ -76,18 +76,16 @@ struct BStage {
 
 // Kernel shapes.  R = register-ring depth (groups whose loads are in flight
 // or waiting to be used), OCC = waves per SIMD the register budget is cut
-// for, NWG = workgroup cap.  Measured on the Llama-3-70B layer: the SwiGLU
-// stream runs a shallow ring at three waves per SIMD, one workgroup per
-// N-block when there are enough N-blocks to fill the chip (no split, so no
-// partials and no fix-up kernel); the shorter projections four groups deep
-// at two waves per SIMD over 512 workgroups (fewer, deeper-ringed
-// workgroups were slower); above 32 rows the accumulators take the
-// registers (one workgroup per CU).
+// for, NWG = workgroup cap.  Measured on the Llama-3-70B layer: three
+// groups deep at two waves per SIMD everywhere (fewer, deeper-ringed
+// workgroups were slower); the SwiGLU stream at up to 32 rows takes one
+// workgroup per N-block when there are enough N-blocks to fill the chip (no
+// split, so no partials and no fix-up kernel).
 struct GemmShape {
   int ring, occ, nwg;
 };
 constexpr GemmShape gemm_shape(int MT, bool swiglu) {
-  return MT > 2 ? GemmShape{4, 1, 256} : swiglu ? GemmShape{3, 2, 768} : GemmShape{3, 2, 512};
+  return MT > 2 ? GemmShape{3, 2, 512} : swiglu ? GemmShape{3, 2, 768} : GemmShape{3, 2, 512};
 }
 constexpr int kRingL = 3;  // LDS ring of activation fragments
 
@@ -354,11 +352,18 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // Activation fragments and group sums are double-buffered: at step i the
   // wave reads unit i + 1's fragments (its LDS slot is complete once the
   // barrier of step i has passed) and applies unit i - 1's sums.
-  half8 af[2][MT][4];
-  f32x4 cs[2][MT][NWV];
-  float sc[2][NWV];
+  // Up to 32 rows the fragments and group sums are double-buffered: at step i
+  // the wave reads unit i + 1's fragments (its LDS slot is complete once the
+  // barrier of step i has passed) and applies unit i - 1's sums.  Above 32
+  // rows the second buffers would cost the second wave per SIMD, so step i
+  // reads, multiplies and applies its own unit.
+  constexpr bool kPipe = MT <= 2;
+  constexpr int kBuf = kPipe ? 2 : 1;
+  half8 af[kBuf][MT][4];
+  f32x4 cs[kBuf][MT][NWV];
+  float sc[kBuf][NWV];
 #pragma unroll
-  for (int q = 0; q < 2; ++q)
+  for (int q = 0; q < kBuf; ++q)
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
       sc[q][nt] = 0.f;
@@ -366,28 +371,35 @@ void w4a16_gemm_kernel(GemmArgs a) {
       for (int mt = 0; mt < MT; ++mt) cs[q][mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   lds_barrier();
-  read_a(0, af[0]);
+  if constexpr (kPipe) read_a(0, af[0]);
   // compute cursor: N-block and group of unit i
   int c_nb = u_lo / G, c_g = u_lo - (u_lo / G) * G;
   for (int i0 = 0; i0 < total; i0 += 2 * kRing) {
 #pragma unroll
     for (int J = 0; J < 2 * kRing; ++J) {
       const int i = i0 + J;
-      const int R = J % kRing, bq = J & 1;
+      const int R = J % kRing, bq = kPipe ? (J & 1) : 0;
       load_a(ar[(R + kRing - 1) % kRing]);
       load_b(bs[(R + kRing - 1) % kRing]);
       advance();
       if (i < total) {
         if (i + 1 < total) store_a((i + 1) % kRingL, ar[(R + 1) % kRing]);
         lds_barrier();
-        if (i + 1 < total) read_a((i + 1) % kRingL, af[bq ^ 1]);
-        mfma_unit(af[bq], bs[R], cs[bq], sc[bq]);
-        apply(cs[bq ^ 1], sc[bq ^ 1]);
+        if constexpr (kPipe) {
+          if (i + 1 < total) read_a((i + 1) % kRingL, af[bq ^ 1]);
+          mfma_unit(af[bq], bs[R], cs[bq], sc[bq]);
+          apply(cs[bq ^ 1], sc[bq ^ 1]);
+        } else {
+          read_a(i % kRingL, af[0]);
+          mfma_unit(af[0], bs[R], cs[0], sc[0]);
+        }
         if (i == total - 1 || c_g == G - 1) {
           apply(cs[bq], sc[bq]);
 #pragma unroll
           for (int nt = 0; nt < NWV; ++nt) sc[bq][nt] = 0.f;
           flush(c_nb);
+        } else if constexpr (!kPipe) {
+          apply(cs[0], sc[0]);
         }
         if (++c_g == G) {
           c_g = 0;
@@ -555,8 +567,8 @@ static void launch_t(const GemmLaunch& L, hipStream_t st) {
     hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks), dim3(256), 0, st, a);
 }
 
-// instantiated shapes: SwiGLU one gate + one up tile per wave; plain two
-// tiles per wave up to 32 rows, one above
+// instantiated shapes: SwiGLU one gate + one up tile per wave; plain one or
+// two tiles per wave
 template <int MT, int EPI>
 static void launch_nw(const GemmLaunch& L, hipStream_t st) {
   if constexpr (EPI == EPI_SWIGLU) {
@@ -565,7 +577,8 @@ static void launch_nw(const GemmLaunch& L, hipStream_t st) {
     if (L.nw == 2) launch_t<MT, 2, EPI>(L, st);
     else launch_t<MT, 1, EPI>(L, st);
   } else {
-    launch_t<MT, 1, EPI>(L, st);
+    if (L.nw == 2) launch_t<MT, 2, EPI>(L, st);
+    else launch_t<MT, 1, EPI>(L, st);
   }
 }
 
@@ -594,7 +607,10 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
     p.nw = 2;  // one gate and one up tile per wave
     p.nblocks = tiles / 4;
   } else {
-    p.nw = (MT <= 2 && tiles % 8 == 0) ? 2 : 1;
+    // above 32 rows two tiles per wave halve the LDS fragment reads per
+    // weight byte, which pays where K is long enough to keep the split-K
+    // partials small
+    p.nw = ((MT <= 2 || K >= 16384) && tiles % 8 == 0) ? 2 : 1;
     p.nblocks = tiles / (4 * p.nw);
   }
   const long units = (long)p.nblocks * (K / 128);

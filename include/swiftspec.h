@@ -157,7 +157,10 @@ int swiftspec_w4a16_swiglu_prepared(const swiftspec_w4* Wg, const swiftspec_w4* 
                                     int32_t M, uint16_t* y, int32_t ldy, void* ws, size_t ws_bytes,
                                     void* stream);
 
-/* out[m][:] = fp16( x[m][:] / sqrt(mean(x[m][:]^2) + eps) * gamma ), M rows of H. */
+/* out[m][:] = fp16( x[m][:] / sqrt(mean(x[m][:]^2) + eps) * gamma ), M rows of H
+ * (the RMSNorm in front of the attention and MLP blocks, and the final norm).
+ * H % 32 == 0 (UNSUPPORTED otherwise); pointers 16-byte aligned, ldx and
+ * ldo multiples of 8. */
 int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, const uint16_t* gamma,
                       float eps, uint16_t* out, int32_t ldo, void* stream);
 

@@ -371,7 +371,7 @@ int swiftspec_w4a16_swiglu_prepared(const swiftspec_w4* Wg, const swiftspec_w4* 
 int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, const uint16_t* gamma,
                       float eps, uint16_t* out, int32_t ldo, void* stream) {
   if (!x || !gamma || !out || M < 0 || H <= 0 || ldx < H || ldo < H) return SWIFTSPEC_INVALID_ARG;
-  if (H % 8) return SWIFTSPEC_UNSUPPORTED;
+  if (H % 32) return SWIFTSPEC_UNSUPPORTED;  // whole 32-element chunks (one operand-layout fragment set)
   if (!aligned16(x) || !aligned16(gamma) || !aligned16(out) || ldx % 8 || ldo % 8)
     return SWIFTSPEC_MISALIGNED;
   if (M == 0) return SWIFTSPEC_OK;

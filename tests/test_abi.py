@@ -78,6 +78,8 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert lib.swiftspec_kv_commit(fake, fake, 2, 100, 8, 64, 128, fake, fake, 8, fake, 0, None, 0,
                                    None) == ss.INVALID_ARG
     assert lib.swiftspec_graph_begin(None) == ss.INVALID_ARG
+    # RMSNorm rows: whole 32-element chunks
+    assert lib.swiftspec_rmsnorm(fake, 4, 72, 72, fake, ctypes.c_float(1e-5), fake, 72, None) == ss.UNSUPPORTED
 
 
 def test_verify_step_rejects_before_launch(ss):

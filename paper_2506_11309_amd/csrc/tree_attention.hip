@@ -223,42 +223,58 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
       }
       s[st] = c;  // lane: keys st*16 + 4*kq + r (r < 4), query row n16
     }
+    // raw scores q.k; the softmax scale and log2 e (c > 0) enter in fp32 at
+    // the exponent, 2^(c s - m); full prefix tiles need no mask
+    const float c2 = a.scale_log2;
     float tmax = -INFINITY;
+    if (!masked && key_end >= kKeyTile) {
 #pragma unroll
-    for (int st = 0; st < 4; ++st)
+      for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kr = st * 16 + 4 * kq + r;
-        bool ok = kr < key_end;
-        if (masked) ok = ok && ((anc >> kr) & 1ull);
-        const float v = ok ? s[st][r] * a.scale_log2 : -INFINITY;
-        s[st][r] = v;
-        tmax = fmaxf(tmax, v);
-      }
+        for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, s[st][r]);
+    } else {
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kr = st * 16 + 4 * kq + r;
+          bool ok = kr < key_end;
+          if (masked) ok = ok && ((anc >> kr) & 1ull);
+          const float v = ok ? s[st][r] : -INFINITY;
+          s[st][r] = v;
+          tmax = fmaxf(tmax, v);
+        }
+    }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-    const float m_new = fmaxf(m_run, tmax);
-    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
+    const float m_new = fmaxf(m_run, tmax * c2);  // base-2 units
+    // reference point of the exponentials: m_new, or 0 while the row has seen
+    // no key (then every exponent is -inf and its 2^x is 0, never NaN)
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
     float psum = 0.f;
     half8 pf[2];
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = (s[st][r] == -INFINITY) ? 0.f : exp2f(s[st][r] - m_new);
-        psum += p;
-        pf[st >> 1][(st & 1) * 4 + r] = (_Float16)p;
+        const float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][r], c2, -m_use));
+        psum += pr;
+        pf[st >> 1][(st & 1) * 4 + r] = (_Float16)pr;
       }
     psum += __shfl_xor(psum, 16, kWave);
     psum += __shfl_xor(psum, 32, kWave);
     l_run = l_run * alpha + psum;
     m_run = m_new;
-    // rescale O: lane holds rows 4*kq + r; fetch those rows' alpha
+    // rescale O (lane holds rows 4*kq + r; fetch those rows' alpha), unless
+    // no row's maximum moved
+    if (__any(alpha != 1.f)) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float ar = __shfl(alpha, 4 * kq + r, kWave);
+      for (int r = 0; r < 4; ++r) {
+        const float ar = __shfl(alpha, 4 * kq + r, kWave);
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[dt][r] *= ar;
+        for (int dt = 0; dt < DT; ++dt) o[dt][r] *= ar;
+      }
     }
     // O += P . V.  A-slot 8 kq + 4 h + r of pf[pp] holds key 32 pp + 16 h +
     // 4 kq + r; the B fragment of d-tile dt needs V[that key][16 dt + n16],

@@ -125,6 +125,18 @@ __device__ __forceinline__ void lds_barrier() {
 
 // Wait until every outstanding memory operation of this wave has completed
 // (stores acknowledged at their coherence scope).
+// Raw buffer resource over [p, p + bytes) (stride 0; dword 3 = the CDNA
+// raw-buffer format), and 16- / 4-byte loads at voffset + soffset from it.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buffer_load_x4(__amdgpu_buffer_rsrc_t r, uint32_t voffset, uint32_t soffset) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voffset, soffset, 0);
+}
+__device__ __forceinline__ uint32_t buffer_load_x1(__amdgpu_buffer_rsrc_t r, uint32_t voffset, uint32_t soffset) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voffset, soffset, 0);
+}
+
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
 
 // Ticket for the deterministic "last arriving workgroup combines" pattern.

@@ -199,21 +199,30 @@ void w4a16_gemm_kernel(GemmArgs a) {
       }
     }
   };
+  // Operand loads go through buffer resources: the wave-uniform part of an
+  // address is a scalar offset and the lane's part a constant vector offset,
+  // so a load costs no vector ALU work.
+  const uint32_t q_bytes = (uint32_t)((size_t)a.K * a.N / 2), sz_bytes = (uint32_t)((size_t)a.N * G * 4);
+  const auto rq0 = buffer_rsrc(a.w0.q, q_bytes), rs0 = buffer_rsrc(a.w0.sz, sz_bytes);
+  const auto rq1 = buffer_rsrc(EPI == EPI_SWIGLU ? a.w1.q : a.w0.q, q_bytes);
+  const auto rs1 = buffer_rsrc(EPI == EPI_SWIGLU ? a.w1.sz : a.w0.sz, sz_bytes);
+  const auto ra = buffer_rsrc(a.a, (uint32_t)(MT * G * 4 * kWave * 16));
+  const uint32_t lane16 = (uint32_t)lane * 16u, col4 = (uint32_t)ncol * 4u;
   auto load_b = [&](BStage<MT, NWV>& st) {
     const int tw = ld_nb * kColB + wave * kColW;  // first column tile of this wave
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
-      const W4Ptr& w = (EPI == EPI_SWIGLU && nt >= kColW) ? a.w1 : a.w0;
-      const size_t tg = (size_t)(tw + nt % kColW) * G + ld_g;
-      st.b[nt] = (w.q + tg * kWave)[lane];
-      st.sz[nt] = (w.sz + tg * 16)[ncol];
+      const bool up = EPI == EPI_SWIGLU && nt >= kColW;
+      const uint32_t tg = (uint32_t)((tw + nt % kColW) * G + ld_g);
+      st.b[nt] = buffer_load_x4(up ? rq1 : rq0, lane16, tg * 1024u);
+      st.sz[nt] = buffer_load_x1(up ? rs1 : rs0, col4, tg * 64u);
     }
   };
   // wave w stages fragment w of every M-tile of the cursor's group
   auto load_a = [&](u32x4 (&r)[MT]) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
-      r[mt] = (reinterpret_cast<const u32x4*>(a.a) + (((size_t)mt * G + ld_g) * 4 + wave) * kWave)[lane];
+      r[mt] = buffer_load_x4(ra, lane16, (uint32_t)(((mt * G + ld_g) * 4 + wave) * 1024));
   };
   auto store_a = [&](int slot, const u32x4 (&r)[MT]) {
 #pragma unroll

@@ -236,6 +236,34 @@ def test_w4a16_swiglu_config_shapes(name):
     check_close(down16(dy), oracle.w4a16_swiglu(Wg, Wu, x), f"swiglu {name}")
 
 
+def _w4_rows(W, rows):
+    """The int4 matrix restricted to output rows (columns of y) `rows`."""
+    return {"qweight": W["qweight"][rows], "scales": W["scales"][rows], "zeros": W["zeros"][rows],
+            "K": W["K"], "N": len(rows)}
+
+
+@pytest.mark.parametrize("M", [32, 9])
+def test_w4a16_swiglu_70b_width(M):
+    """SwiGLU at the 70B FFN width (K = 8192, N = 28672), checked against the
+    oracle on every column of four 112-column stretches (first, second, a
+    middle one, last) and on 256 random columns."""
+    K, N = 8192, 28672
+    Wg, Wu = _rand_w4(21, N, K), _rand_w4(22, N, K)
+    x = gen.normal_f16(23, 0, (M, K))
+    tg, dg = upload_w4(Wg)
+    tu, du = upload_w4(Wu)
+    dy = torch.zeros((M, N), dtype=torch.int16, device=dev())
+    ws = ss.workspace(ss.swiglu_workspace_bytes(M, K, N), dev())
+    ss.w4a16_swiglu(dg, du, up(x), dy, ws)
+    torch.cuda.synchronize()
+    y = down16(dy)
+    blk = 7 * 16
+    cols = np.concatenate([np.arange(b * blk, (b + 1) * blk) for b in (0, 1, 128, N // blk - 1)]
+                          + [np.random.default_rng(24).choice(N, 256, replace=False)])
+    ref = oracle.w4a16_swiglu(_w4_rows(Wg, cols), _w4_rows(Wu, cols), x)
+    check_close(y[:, cols], ref, f"swiglu 70b width M={M}")
+
+
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 1024), (8, 2048, 512), (13, 1024, 2048), (32, 8192, 1024),
                                    (40, 4096, 1024), (64, 2048, 1024)])
 def test_w4a16_gemm_valu_variant_matches_oracle(M, K, N):

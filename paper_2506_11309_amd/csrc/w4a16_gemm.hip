@@ -18,8 +18,10 @@
 //     (1024 + 16 z) leaves q - z (16 (q - z)) exactly.  Low-nibble slots
 //     meet activations pre-multiplied by 16, so every product is
 //     16 x (q - z) exactly and the MFMA sum of a group is
-//     C_g = 16 sum_k x (q - z); per group y += (s / 16) C_g (one FMA per
-//     output element).
+//     C_g = 16 sum_k x (q - z).  Per group the accumulator takes s C_g (one
+//     mixed-precision FMA per output element, fp16 s read in place), and
+//     the block's sum is multiplied by 1/16 once at its end (exact: a power
+//     of two), which equals summing (s / 16) C_g.
 //   * Stream-K scheduling: a fixed grid of workgroups (4 waves each) splits
 //     the (N-block, group) iteration space into equal contiguous ranges; the
 //     4 waves split an N-block's columns.  Per group, every wave loads 1 KB
@@ -240,7 +242,7 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // (1024 + 16 q, ...); subtracting 1024 + z (resp. 1024 + 16 z) leaves
   // q - z (resp. 16 (q - z)) exactly.  Low-nibble slots meet activations
   // pre-multiplied by 16, so the MFMA sum of a group is C_g = 16 sum_k x (q - z)
-  // and y += (s / 16) C_g.
+  // and the accumulator takes s C_g (scaled by 1/16 when the block ends).
   // The magic constant is kept in a register (opaque to the optimiser) so
   // that mask-and-insert is one v_bfi_b32 with the mask in a scalar register.
   uint32_t magic = 0x64006400u;
@@ -254,11 +256,11 @@ void w4a16_gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int f = 0; f < 4; ++f) af[mt][f] = bitcast<half8>(abuf[slot][mt][f][lane]);
   };
-  // group sums C_g of one unit (and the tiles' s / 16); applied to the
+  // group sums C_g of one unit (and the tiles' scale words); applied to the
   // accumulators one step later, so that no instruction waits on the MFMAs
   // just issued
   auto mfma_unit = [&](const half8 (&af)[MT][4], const BStage<MT, NWV>& st, f32x4 (&c)[MT][NWV],
-                       float (&s16)[NWV]) {
+                       uint32_t (&sw)[NWV]) {
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
       const u32x4 w = st.b[nt];
@@ -271,7 +273,7 @@ void w4a16_gemm_kernel(GemmArgs a) {
       const half8 blo_b = bitcast<half8>(u32x4{deq(w[2], kLo, zlo), deq(s2, kLo, zlo), deq(w[3], kLo, zlo), deq(s3, kLo, zlo)});
       const half8 bhi_a = bitcast<half8>(u32x4{deq(w[0], kHi, zhi), deq(s0, kHi, zhi), deq(w[1], kHi, zhi), deq(s1, kHi, zhi)});
       const half8 bhi_b = bitcast<half8>(u32x4{deq(w[2], kHi, zhi), deq(s2, kHi, zhi), deq(w[3], kHi, zhi), deq(s3, kHi, zhi)});
-      s16[nt] = h2f((uint16_t)(st.sz[nt] & 0xFFFFu)) * 0.0625f;
+      sw[nt] = st.sz[nt];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 cc = {0.f, 0.f, 0.f, 0.f};
@@ -283,13 +285,14 @@ void w4a16_gemm_kernel(GemmArgs a) {
       }
     }
   };
-  auto apply = [&](const f32x4 (&c)[MT][NWV], const float (&s16)[NWV]) {
+  auto apply = [&](const f32x4 (&c)[MT][NWV], const uint32_t (&sw)[NWV]) {
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[mt][nt][r] = __builtin_fmaf(c[mt][nt][r], s16[nt], acc[mt][nt][r]);
+        for (int r = 0; r < 4; ++r)
+          acc[mt][nt][r] = __builtin_fmaf(c[mt][nt][r], (float)bitcast<half2v>(sw[nt])[0], acc[mt][nt][r]);
   };
 
   auto emit = [&](int nb) {
@@ -311,6 +314,10 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // range holds the whole N-block, else publish the partial (slot 0: the
   // range's first N-block, slot 1: its last) for the fix-up kernel.
   auto flush = [&](int nb) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] *= 0.0625f;  // the 16 of C_g, exactly
     const bool full = (long)nb * G >= u_lo && (long)(nb + 1) * G <= u_hi;
     if (full) {
       emit(nb);
@@ -370,12 +377,12 @@ void w4a16_gemm_kernel(GemmArgs a) {
   constexpr int kBuf = kPipe ? 2 : 1;
   half8 af[kBuf][MT][4];
   f32x4 cs[kBuf][MT][NWV];
-  float sc[kBuf][NWV];
+  uint32_t sc[kBuf][NWV];
 #pragma unroll
   for (int q = 0; q < kBuf; ++q)
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
-      sc[q][nt] = 0.f;
+      sc[q][nt] = 0u;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) cs[q][mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -405,7 +412,7 @@ void w4a16_gemm_kernel(GemmArgs a) {
         if (i == total - 1 || c_g == G - 1) {
           apply(cs[bq], sc[bq]);
 #pragma unroll
-          for (int nt = 0; nt < NWV; ++nt) sc[bq][nt] = 0.f;
+          for (int nt = 0; nt < NWV; ++nt) sc[bq][nt] = 0u;
           flush(c_nb);
         } else if constexpr (!kPipe) {
           apply(cs[0], sc[0]);

@@ -365,9 +365,6 @@ void w4a16_gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) asm volatile("" : : "v"(r[mt]));
   };
-  // Activation fragments and group sums are double-buffered: at step i the
-  // wave reads unit i + 1's fragments (its LDS slot is complete once the
-  // barrier of step i has passed) and applies unit i - 1's sums.
   // Up to 32 rows the fragments and group sums are double-buffered: at step i
   // the wave reads unit i + 1's fragments (its LDS slot is complete once the
   // barrier of step i has passed) and applies unit i - 1's sums.  Above 32

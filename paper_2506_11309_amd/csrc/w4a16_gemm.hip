@@ -80,7 +80,7 @@ struct BStage {
 // or waiting to be used), OCC = waves per SIMD the register budget is cut
 // for, NWG = workgroup cap.  Measured on the Llama-3-70B layer: three
 // groups deep at two waves per SIMD everywhere (fewer, deeper-ringed
-// workgroups were slower); the SwiGLU stream at up to 32 rows takes one
+// workgroups were slower); the SwiGLU stream takes one
 // workgroup per N-block when there are enough N-blocks to fill the chip (no
 // split, so no partials and no fix-up kernel).
 struct GemmShape {
@@ -628,8 +628,10 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
   }
   const long units = (long)p.nblocks * (K / 128);
   int cap = gemm_shape(MT, swiglu).nwg;
-  // whole N-blocks per workgroup when they alone fill the chip
-  if (swiglu && MT <= 2 && p.nblocks >= 256 && p.nblocks <= 2 * cap) cap = p.nblocks;
+  // whole N-blocks per workgroup when they alone fill the chip (the SwiGLU
+  // at the 70B width: 448 blocks; at 48 and 64 rows 11 % faster than
+  // stream-K, whose gate and up partials cost a 16 us fix-up at 64 rows)
+  if (swiglu && p.nblocks >= 256 && p.nblocks <= 2 * cap) cap = p.nblocks;
   p.nwg = (int)(units < cap ? units : cap);
   const int col_w = swiglu ? p.nw / 2 : p.nw;
   const int src = swiglu ? 2 : 1;

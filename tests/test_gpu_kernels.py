@@ -242,7 +242,7 @@ def _w4_rows(W, rows):
             "K": W["K"], "N": len(rows)}
 
 
-@pytest.mark.parametrize("M", [32, 9])
+@pytest.mark.parametrize("M", [32, 9, 64, 47])
 def test_w4a16_swiglu_70b_width(M):
     """SwiGLU at the 70B FFN width (K = 8192, N = 28672), checked against the
     oracle on every column of four 112-column stretches (first, second, a

@@ -55,6 +55,25 @@ struct AttnArgs {
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
+// Reduction over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the four key
+// quarters of one query row in the score layout), in registers: with both
+// operands holding x, v_permlane16_swap_b32 leaves 16-lane rows (0, 0, 2, 2)
+// of x in the first register and rows (1, 1, 3, 3) in the second, and
+// v_permlane32_swap_b32 leaves the lower half twice and the upper half
+// twice, so op over the two registers after each swap reduces first across
+// lane ^ 16, then across lane ^ 32.  (The s_nop covers the wait states a
+// permlane needs after a vector ALU write of its operands.)
+template <class Op>
+__device__ __forceinline__ float quarter_reduce(float x, Op op) {
+  uint32_t a = bitcast<uint32_t>(x), b = a;
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+  x = op(bitcast<float>(a), bitcast<float>(b));
+  a = bitcast<uint32_t>(x);
+  b = a;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+  return op(bitcast<float>(a), bitcast<float>(b));
+}
+
 // Bytes of one workgroup's partial: O normalised by its row sum, fp16
 // [W waves][D/16 d-tiles][64 lanes][4 rows], then the fp32 base-2
 // log-sum-exp m + log2(l) of its 16 W rows (-inf for a row that saw no
@@ -203,7 +222,10 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
     }
   }
 
-  float m_run = -INFINITY, l_run = 0.f;  // for row n16 of this wave (replicated over kq)
+  // running maximum of row n16 (the same in its four lanes) and this lane's
+  // share of the row's running sum (its 16 keys of every tile); the shares
+  // are added once, at the end
+  float m_run = -INFINITY, l_run = 0.f;
   f32x4 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -245,26 +267,26 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
           tmax = fmaxf(tmax, v);
         }
     }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+    tmax = quarter_reduce(tmax, [](float x, float y) { return fmaxf(x, y); });
     const float m_new = fmaxf(m_run, tmax * c2);  // base-2 units
     // reference point of the exponentials: m_new, or 0 while the row has seen
     // no key (then every exponent is -inf and its 2^x is 0, never NaN)
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
+    float pr[16];
     half8 pf[2];
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][r], c2, -m_use));
-        psum += pr;
-        pf[st >> 1][(st & 1) * 4 + r] = (_Float16)pr;
+        pr[st * 4 + r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][r], c2, -m_use));
+        pf[st >> 1][(st & 1) * 4 + r] = (_Float16)pr[st * 4 + r];
       }
-    psum += __shfl_xor(psum, 16, kWave);
-    psum += __shfl_xor(psum, 32, kWave);
-    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int w = 1; w < 16; w *= 2)  // pairwise sum of the lane's 16 keys
+#pragma unroll
+      for (int e = 0; e < 16; e += 2 * w) pr[e] += pr[e + w];
+    l_run = l_run * alpha + pr[0];
     m_run = m_new;
     // rescale O (lane holds rows 4*kq + r; fetch those rows' alpha), unless
     // no row's maximum moved
@@ -374,6 +396,7 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
   }
 
   // ---- publish this split's partial (merged by the next kernel) ----
+  l_run = quarter_reduce(l_run, [](float x, float y) { return x + y; });
   float inv[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {

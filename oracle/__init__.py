@@ -64,6 +64,8 @@ def _load():
     lib.oracle_verify_layer.restype = ctypes.c_int
     lib.oracle_lm_head.argtypes = [vp, i32, i32, vp, dbl, vp, i32, vp]
     lib.oracle_lm_head.restype = ctypes.c_int
+    lib.oracle_greedy_accept.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.oracle_greedy_accept.restype = i32
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -230,6 +232,23 @@ def lm_head(h, gamma, W, eps=1e-5):
     if rc != 0:
         raise ValueError("oracle_lm_head: invalid arguments")
     return out
+
+
+def greedy_accept(logits, tokens, parent):
+    """Greedy acceptance of a verified tree: (argmax[T], accepted node, bonus
+    token, accepted path length L)."""
+    lg = _c(logits, np.uint16)
+    T, V = lg.shape
+    tok = _c(tokens, np.int32)
+    p = _c(parent, np.int32)
+    assert len(tok) == T and len(p) == T
+    am = np.empty(T, np.int32)
+    acc = np.zeros(1, np.int32)
+    bon = np.zeros(1, np.int32)
+    L = _load().oracle_greedy_accept(_p(lg), T, V, V, _p(tok), _p(p), _p(am), _p(acc), _p(bon))
+    if L < 0:
+        raise ValueError("oracle_greedy_accept: invalid arguments or tree")
+    return am, int(acc[0]), int(bon[0]), int(L)
 
 
 def num_threads() -> int:

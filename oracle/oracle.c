@@ -315,6 +315,47 @@ int32_t oracle_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
   return L;
 }
 
+/* -------------------------------------------------------- greedy acceptance */
+
+int32_t oracle_greedy_accept(const uint16_t* logits, int32_t T, int32_t V, int32_t ldl,
+                             const int32_t* tokens, const int32_t* parent, int32_t* argmax,
+                             int32_t* accepted, int32_t* bonus) {
+  if (T < 1 || V < 1 || ldl < V) return -1;
+  if (oracle_tree(parent, T, NULL, NULL) != 0) return -1;
+  /* the target's greedy choice after each node: the first vocabulary index
+   * holding the row's largest logit */
+  for (int32_t i = 0; i < T; ++i) {
+    const uint16_t* row = logits + (size_t)i * ldl;
+    int32_t best = 0;
+    double bv = oracle_f16_to_f64(row[0]);
+    for (int32_t v = 1; v < V; ++v) {
+      const double x = oracle_f16_to_f64(row[v]);
+      if (x > bv) {
+        bv = x;
+        best = v;
+      }
+    }
+    argmax[i] = best;
+  }
+  /* walk from the root: the next accepted node is the lowest-index child
+   * whose draft token is the target's choice after the current node */
+  int32_t u = 0, L = 1;
+  for (;;) {
+    int32_t next = -1;
+    for (int32_t c = 1; c < T; ++c)
+      if (parent[c] == u && tokens[c] == argmax[u]) {
+        next = c;
+        break;
+      }
+    if (next < 0) break;
+    u = next;
+    ++L;
+  }
+  *accepted = u;
+  *bonus = argmax[u];
+  return L;
+}
+
 /* ------------------------------------------------------------------- layer */
 
 int oracle_verify_layer(const oracle_dims* dims, const uint16_t* attn_norm,

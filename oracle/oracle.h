@@ -88,6 +88,19 @@ int32_t oracle_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
                          int64_t layer_stride, int32_t Hkv, int32_t S_max, int32_t D, int32_t P,
                          const int32_t* parent, int32_t T, int32_t accepted);
 
+/* Greedy acceptance of a verified tree (target-side verification with the
+ * target's greedy choice; Sec. 3.1, Fig. 3 walk-through).  logits [T][ldl]
+ * fp16: row i is the target's distribution after the path root -> node i.
+ * argmax[i] = first index of the largest logit of row i.  From the root,
+ * repeatedly step to the lowest-index child c with tokens[c] == argmax of
+ * the current node; the node where no child matches is *accepted and its
+ * argmax is the *bonus token.  tokens[0] (the root's own token) is not
+ * used.  Returns L = depth(accepted) + 1 (accepted path length, root
+ * included), or -1 for invalid arguments or tree. */
+int32_t oracle_greedy_accept(const uint16_t* logits, int32_t T, int32_t V, int32_t ldl,
+                             const int32_t* tokens, const int32_t* parent, int32_t* argmax,
+                             int32_t* accepted, int32_t* bonus);
+
 typedef struct {
   int32_t H, Hq, Hkv, D, F, S_max;
   double eps, rope_theta;

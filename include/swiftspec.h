@@ -223,6 +223,36 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
                         const int32_t* d_accepted_node, int32_t advance, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------- greedy acceptance
+ * Closes a verification step on the device (Sec. 3.1, Fig. 3 walk-through:
+ * an iteration's output is the accepted root path followed by one token
+ * the target produced after it), for the target's greedy choice.
+ *   logits  [T][ldl] fp16 (device): row i = the target's scores for the
+ *           token after the root path of node i (as written by
+ *           swiftspec_verify_step / swiftspec_lm_head); V columns are read;
+ *           values are expected to be finite.
+ *   d_tokens[T] int32: the draft token of each node (d_tokens[0], the
+ *           root's own token, is not read).
+ *   d_parent[T] int32: the tree (parent[0] = -1, 0 <= parent[i] < i).
+ * Outputs (device int32): d_argmax[i] = the first index of row i's largest
+ * value (the target's choice after node i); *d_accepted = the node reached
+ * from the root by repeatedly stepping to the lowest-index child whose
+ * token equals the current node's choice, stopping where no child matches;
+ * *d_bonus = d_argmax[*d_accepted]; *d_path_len (nullable) = depth of the
+ * accepted node + 1 (the accepted path, root included).  The accepted node
+ * can be passed straight to swiftspec_kv_commit (d_accepted_node) on the
+ * same stream, so verify, accept and commit replay as one graph.
+ * 1 <= T <= 64, ldl >= V, ldl % 8 == 0, logits 16-byte aligned.  ws: a
+ * workspace of swiftspec_greedy_accept_workspace_bytes(T) bytes (its
+ * header's first ticket counter is used and left zero).  An invalid tree
+ * sets SWIFTSPEC_DEVERR_BAD_TREE; d_argmax is still written, the other
+ * outputs are not. */
+size_t swiftspec_greedy_accept_workspace_bytes(int32_t T);
+int swiftspec_greedy_accept(const uint16_t* logits, int32_t ldl, int32_t T, int32_t V,
+                            const int32_t* d_tokens, const int32_t* d_parent, int32_t* d_argmax,
+                            int32_t* d_accepted, int32_t* d_bonus, int32_t* d_path_len, void* ws,
+                            size_t ws_bytes, void* stream);
+
 /* -------------------------------------------------------- decoder layer */
 typedef struct {
   int32_t H, Hq, Hkv, D, F, S_max;

@@ -58,6 +58,8 @@ _SIGS = {
     "swiftspec_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "swiftspec_last_hip_error": ([], ctypes.c_int),
     "swiftspec_workspace_init": ([vp, sz, vp], ctypes.c_int),
+    "swiftspec_greedy_accept_workspace_bytes": ([i32], sz),
+    "swiftspec_greedy_accept": ([vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     "swiftspec_read_device_error": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
     "swiftspec_w4_packed_bytes": ([i32, i32], sz),
     "swiftspec_w4_prepack": ([ctypes.POINTER(W4), vp, sz, vp], ctypes.c_int),
@@ -298,6 +300,23 @@ def kv_commit(k_cache, v_cache, prefix_len, parent, accepted, n_layers=1, layer_
                                      int(bool(advance)), _ptr(ws), ws.numel() if ws is not None else 0,
                                      _stream(stream))
     _check(st, "kv_commit")
+
+
+def greedy_accept_workspace_bytes(T) -> int:
+    return int(_load().swiftspec_greedy_accept_workspace_bytes(T))
+
+
+def greedy_accept(logits, tokens, parent, argmax, accepted, bonus, ws, path_len=None, V=None,
+                  stream=None):
+    """logits [T][ldl] fp16 (first V columns; default all); tokens, parent
+    [T] and the outputs argmax [T], accepted, bonus, path_len [1] are device
+    int32 tensors."""
+    T, ldl = logits.shape
+    st = _load().swiftspec_greedy_accept(_ptr(logits), ldl, T, ldl if V is None else V, _ptr(tokens),
+                                         _ptr(parent), _ptr(argmax), _ptr(accepted), _ptr(bonus),
+                                         _ptr(path_len), _ptr(ws), ws.numel() if ws is not None else 0,
+                                         _stream(stream))
+    _check(st, "greedy_accept")
 
 
 def make_dims(H, Hq, Hkv, D, F, S_max, eps=1e-5, rope_theta=500000.0) -> Dims:

@@ -454,6 +454,26 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
   return check_launch();
 }
 
+size_t swiftspec_greedy_accept_workspace_bytes(int32_t T) {
+  (void)T;
+  return kHeader;
+}
+
+int swiftspec_greedy_accept(const uint16_t* logits, int32_t ldl, int32_t T, int32_t V,
+                            const int32_t* d_tokens, const int32_t* d_parent, int32_t* d_argmax,
+                            int32_t* d_accepted, int32_t* d_bonus, int32_t* d_path_len, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if (!logits || !d_tokens || !d_parent || !d_argmax || !d_accepted || !d_bonus || !ws)
+    return SWIFTSPEC_INVALID_ARG;
+  if (T < 1 || V < 1 || ldl < V) return SWIFTSPEC_INVALID_ARG;
+  if (T > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(logits) || ldl % 8) return SWIFTSPEC_MISALIGNED;
+  if (ws_bytes < kHeader) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  ss::launch_greedy_accept(logits, ldl, T, V, d_tokens, d_parent, d_argmax, d_accepted, d_bonus, d_path_len,
+                           ws, S(stream));
+  return check_launch();
+}
+
 size_t swiftspec_verify_layer_workspace_bytes(const swiftspec_dims* dims, int32_t T) {
   if (!dims || T < 1 || T > SWIFTSPEC_MAX_TREE) return kHeader;
   return layer_ws(dims, T).total;

@@ -80,6 +80,18 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert lib.swiftspec_graph_begin(None) == ss.INVALID_ARG
     # RMSNorm rows: whole 32-element chunks
     assert lib.swiftspec_rmsnorm(fake, 4, 72, 72, fake, ctypes.c_float(1e-5), fake, 72, None) == ss.UNSUPPORTED
+    # greedy acceptance: sizes, leading dimension, workspace, null outputs
+    acc = lambda T, V, ldl, lg=fake, ws=fake, wsb=1 << 20, bonus=fake: lib.swiftspec_greedy_accept(
+        lg, ldl, T, V, fake, fake, fake, fake, bonus, None, ws, wsb, None)
+    assert acc(0, 1000, 1000) == ss.INVALID_ARG
+    assert acc(65, 1000, 1000) == ss.UNSUPPORTED
+    assert acc(8, 1000, 999) == ss.INVALID_ARG
+    assert acc(8, 1000, 1004) == ss.MISALIGNED
+    assert acc(8, 1000, 1000, lg=fake + 4) == ss.MISALIGNED
+    assert acc(8, 1000, 1000, wsb=16) == ss.WORKSPACE_TOO_SMALL
+    assert acc(8, 1000, 1000, ws=None) == ss.INVALID_ARG
+    assert acc(8, 1000, 1000, bonus=None) == ss.INVALID_ARG
+    assert lib.swiftspec_greedy_accept_workspace_bytes(64) == ss.WS_HEADER_BYTES
 
 
 def test_verify_step_rejects_before_launch(ss):

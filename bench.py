@@ -316,7 +316,9 @@ def full_step(args, ss, torch, np, dev, stream):
     layer's own weights and caches (35.8 GB of int4 weights + 2.1 GB LM head
     + 2.7 GB of KV cache, drawn on the device with the workload recipe), the
     graph replayed `full_step_reps` times and timed with HIP events; the
-    KV commit of the accepted path over all 80 layers timed as one launch."""
+    KV commit of the accepted path over all 80 layers timed as one launch;
+    the greedy acceptance alone, and the closed step (verification, greedy
+    acceptance and the commit of the path it accepts) as one graph."""
     from gen import device as gdev
     from gen import workloads as wl
     cfg = wl.CONFIGS["c5"]
@@ -355,14 +357,24 @@ def full_step(args, ss, torch, np, dev, stream):
     ws = ss.workspace(ss.verify_step_workspace_bytes(dims, T, cfg.vocab), dev)
     hidden = torch.empty_like(x)
     logits = torch.zeros((T, cfg.vocab), dtype=torch.int16, device=dev)
+    # draft tokens of the tree nodes (seeded, uniform over the vocabulary)
+    tokens = torch.from_numpy(np.random.default_rng(cfg.seeds()["tree"]).integers(0, cfg.vocab, T)
+                              .astype(np.int32)).to(dev)
+    d_am = torch.zeros(T, dtype=torch.int32, device=dev)
+    d_acc, d_bonus, d_len = (torch.zeros(1, dtype=torch.int32, device=dev) for _ in range(3))
+    aws = ss.workspace(ss.greedy_accept_workspace_bytes(T), dev)
     torch.cuda.synchronize()
     setup_s = time.time() - t0
 
-    def timed(enqueue, reps, warm=2):
+    def timed(enqueue, reps, warm=2, inner=1):
+        # `inner` back-to-back copies in one graph, per-copy times returned:
+        # a launch of a few microseconds alone would time the host's graph
+        # submission rather than the kernel
         g = ss.Graph()
         with torch.cuda.stream(stream):
             g.begin(stream)
-            enqueue()
+            for _ in range(inner):
+                enqueue()
             g.end(stream)
             for _ in range(warm):
                 g.launch(stream)
@@ -372,7 +384,7 @@ def full_step(args, ss, torch, np, dev, stream):
                 g.launch(stream)
                 ev[i + 1].record(stream)
         ev[-1].synchronize()
-        return sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(reps))
+        return sorted(ev[i].elapsed_time(ev[i + 1]) / inner for i in range(reps))
 
     def step():
         hidden.copy_(x)  # the tree tokens' embeddings enter the step
@@ -383,7 +395,21 @@ def full_step(args, ss, torch, np, dev, stream):
         raise RuntimeError("device error in the 80-layer step")
     head_ms = timed(lambda: ss.lm_head(hidden, gamma, lm_w, logits, ws, stream=stream), args.full_step_reps)
     commit_ms = timed(lambda: ss.kv_commit(kc, vc, P_dev, dparent, dacc, n_layers=nl, advance=False, ws=ws,
-                                           stream=stream), args.full_step_reps)
+                                           stream=stream), args.full_step_reps, inner=20)
+
+    def accept():
+        ss.greedy_accept(logits, tokens, dparent, d_am, d_acc, d_bonus, aws, path_len=d_len, stream=stream)
+
+    accept_ms = timed(accept, args.full_step_reps, inner=20)
+
+    def closed_step():
+        step()
+        accept()
+        ss.kv_commit(kc, vc, P_dev, dparent, d_acc, n_layers=nl, advance=False, ws=aws, stream=stream)
+
+    closed_ms = timed(closed_step, args.full_step_reps)
+    if ss.read_device_error(aws, stream):
+        raise RuntimeError("device error in the closed step")
     med = lambda v: v[len(v) // 2]
     w_bytes = nl * s.w4_bytes()
     kv_bytes = nl * cfg.kv_bytes_per_layer()
@@ -401,6 +427,9 @@ def full_step(args, ss, torch, np, dev, stream):
            "lm_head_us": round(med(head_ms) * 1000.0, 2),
            "lm_head_gbs": round((head_bytes + T * s.H * 4) / (med(head_ms) * 1e-3) / 1e9, 1),
            "kv_commit_all_layers_us": round(med(commit_ms) * 1000.0, 2),
+           "greedy_accept_us": round(med(accept_ms) * 1000.0, 2),
+           "ms_per_step_closed": round(sum(closed_ms) / len(closed_ms), 4),
+           "closed_step": "verification + greedy acceptance + commit of the accepted path, one graph",
            "reps": args.full_step_reps, "setup_s": round(setup_s, 1),
            "weights": "drawn on the device with the workload recipe (torch generator, seeded)"}
     del keep, kc, vc, lm_w

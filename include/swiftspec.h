@@ -243,10 +243,10 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
  * can be passed straight to swiftspec_kv_commit (d_accepted_node) on the
  * same stream, so verify, accept and commit replay as one graph.
  * 1 <= T <= 64, ldl >= V, ldl % 8 == 0, logits 16-byte aligned.  ws: a
- * workspace of swiftspec_greedy_accept_workspace_bytes(T) bytes (its
- * header's first ticket counter is used and left zero).  An invalid tree
- * sets SWIFTSPEC_DEVERR_BAD_TREE; d_argmax is still written, the other
- * outputs are not. */
+ * workspace of swiftspec_greedy_accept_workspace_bytes(T) bytes (per-range
+ * partial maxima after the header; the header's first ticket counter is
+ * used and left zero).  An invalid tree sets SWIFTSPEC_DEVERR_BAD_TREE;
+ * d_argmax is still written, the other outputs are not. */
 size_t swiftspec_greedy_accept_workspace_bytes(int32_t T);
 int swiftspec_greedy_accept(const uint16_t* logits, int32_t ldl, int32_t T, int32_t V,
                             const int32_t* d_tokens, const int32_t* d_parent, int32_t* d_argmax,

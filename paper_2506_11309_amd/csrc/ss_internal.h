@@ -91,9 +91,10 @@ void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc
 
 void launch_ws_init(void* ws, size_t bytes, hipStream_t st);
 
+int greedy_accept_splits(int T);  // workgroups per logits row
 void launch_greedy_accept(const uint16_t* logits, int ldl, int T, int V, const int32_t* tokens,
                           const int32_t* parent, int32_t* argmax, int32_t* accepted, int32_t* bonus,
-                          int32_t* path_len, void* ws, hipStream_t st);
+                          int32_t* path_len, void* ws, void* part, hipStream_t st);
 void launch_lm_head(const uint16_t* xn, int M, int H, const uint16_t* W, int V, uint16_t* logits, int ldl,
                     hipStream_t st);
 

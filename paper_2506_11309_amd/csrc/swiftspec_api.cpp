@@ -455,8 +455,8 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
 }
 
 size_t swiftspec_greedy_accept_workspace_bytes(int32_t T) {
-  (void)T;
-  return kHeader;
+  if (T < 1 || T > SWIFTSPEC_MAX_TREE) return kHeader;
+  return kHeader + align_up((size_t)T * ss::greedy_accept_splits(T) * 8);
 }
 
 int swiftspec_greedy_accept(const uint16_t* logits, int32_t ldl, int32_t T, int32_t V,
@@ -468,9 +468,9 @@ int swiftspec_greedy_accept(const uint16_t* logits, int32_t ldl, int32_t T, int3
   if (T < 1 || V < 1 || ldl < V) return SWIFTSPEC_INVALID_ARG;
   if (T > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_UNSUPPORTED;
   if (!aligned16(logits) || ldl % 8) return SWIFTSPEC_MISALIGNED;
-  if (ws_bytes < kHeader) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  if (ws_bytes < swiftspec_greedy_accept_workspace_bytes(T)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   ss::launch_greedy_accept(logits, ldl, T, V, d_tokens, d_parent, d_argmax, d_accepted, d_bonus, d_path_len,
-                           ws, S(stream));
+                           ws, static_cast<char*>(ws) + kHeader, S(stream));
   return check_launch();
 }
 

@@ -64,6 +64,8 @@ def _load():
     lib.oracle_verify_layer.restype = ctypes.c_int
     lib.oracle_lm_head.argtypes = [vp, i32, i32, vp, dbl, vp, i32, vp]
     lib.oracle_lm_head.restype = ctypes.c_int
+    lib.oracle_kv_reorganize.argtypes = [vp, vp, i32, i64, i32, i32, i32, i32, vp, i32, i32, i32, vp, vp]
+    lib.oracle_kv_reorganize.restype = i32
     lib.oracle_greedy_accept.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.oracle_greedy_accept.restype = i32
     lib.oracle_num_threads.argtypes = []
@@ -232,6 +234,25 @@ def lm_head(h, gamma, W, eps=1e-5):
     if rc != 0:
         raise ValueError("oracle_lm_head: invalid arguments")
     return out
+
+
+def kv_reorganize(k_cache, v_cache, P, parent, last, keep=True, n_layers=1, layer_stride=None):
+    """Draft-side reorganisation in place on [n_layers][Hkv][S_max][D] (or
+    [Hkv][S_max][D]) caches; returns (L, new_parent of the kept nodes)."""
+    p = _c(parent, np.int32)
+    assert k_cache.flags["C_CONTIGUOUS"] and v_cache.flags["C_CONTIGUOUS"]
+    Hkv, S_max, D = k_cache.shape[-3:]
+    if layer_stride is None:
+        layer_stride = Hkv * S_max * D
+    N = len(p)
+    newp = np.empty(max(N, 1), np.int32)
+    S = np.zeros(1, np.int32)
+    L = _load().oracle_kv_reorganize(_p(k_cache), _p(v_cache), n_layers, layer_stride, Hkv, S_max, D, P,
+                                     _p(p if N else np.zeros(1, np.int32)), N, int(last), int(bool(keep)),
+                                     _p(newp), _p(S))
+    if L < 0:
+        raise ValueError("oracle_kv_reorganize: invalid arguments or forest")
+    return int(L), newp[:int(S[0])].copy()
 
 
 def greedy_accept(logits, tokens, parent):

@@ -315,6 +315,59 @@ int32_t oracle_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
   return L;
 }
 
+/* ------------------------------------------- draft-side KV reorganisation */
+
+int32_t oracle_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers, int64_t layer_stride,
+                             int32_t Hkv, int32_t S_max, int32_t D, int32_t P, const int32_t* parent,
+                             int32_t N, int32_t last, int32_t keep, int32_t* new_parent, int32_t* n_kept) {
+  if (n_layers < 1 || Hkv < 1 || D < 1 || N < 0 || P < 0 || P + N > S_max) return -1;
+  if (layer_stride < (int64_t)Hkv * S_max * D) return -1;
+  if (last < -1 || last >= N) return -1;
+  for (int32_t i = 0; i < N; ++i)
+    if (parent[i] < -1 || parent[i] >= i) return -1;
+  /* the verified path inside the forest: its root ... last */
+  int32_t* order = (int32_t*)malloc(sizeof(int32_t) * (N > 0 ? N : 1));
+  int32_t L = 0;
+  for (int32_t j = last; j != -1; j = parent[j]) order[L++] = j;
+  for (int32_t i = 0; i < L / 2; ++i) {
+    const int32_t t = order[i];
+    order[i] = order[L - 1 - i];
+    order[L - 1 - i] = t;
+  }
+  /* the subtree below last, in index order (a node is kept when last is
+   * one of its ancestors) */
+  int32_t S = 0;
+  if (keep && last >= 0)
+    for (int32_t c = last + 1; c < N; ++c) {
+      int32_t below = 0;
+      for (int32_t j = parent[c]; j != -1; j = parent[j])
+        if (j == last) below = 1;
+      if (below) {
+        int32_t pos = -1;
+        if (parent[c] != last)
+          for (int32_t q = 0; q < S; ++q)
+            if (order[L + q] == parent[c]) pos = q;
+        new_parent[S] = pos;
+        order[L + S++] = c;
+      }
+    }
+  uint16_t* snap = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(N > 0 ? N : 1) * D);
+  for (int32_t layer = 0; layer < n_layers; ++layer)
+    for (int32_t which = 0; which < 2; ++which) {
+      uint16_t* cache = (which ? v_cache : k_cache) + (size_t)layer * layer_stride;
+      for (int32_t g = 0; g < Hkv; ++g) {
+        uint16_t* tree_rows = cache + ((size_t)g * S_max + P) * D;
+        memcpy(snap, tree_rows, sizeof(uint16_t) * (size_t)N * D);
+        for (int32_t i = 0; i < L + S; ++i)
+          memcpy(tree_rows + (size_t)i * D, snap + (size_t)order[i] * D, sizeof(uint16_t) * D);
+      }
+    }
+  free(order);
+  free(snap);
+  *n_kept = S;
+  return L;
+}
+
 /* -------------------------------------------------------- greedy acceptance */
 
 int32_t oracle_greedy_accept(const uint16_t* logits, int32_t T, int32_t V, int32_t ldl,

@@ -88,6 +88,20 @@ int32_t oracle_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
                          int64_t layer_stride, int32_t Hkv, int32_t S_max, int32_t D, int32_t P,
                          const int32_t* parent, int32_t T, int32_t accepted);
 
+/* Draft-side KV reorganisation after re-rooting (Sec. 3.2, consistency
+ * management of the draft model's cache; Fig. 5).  Rows [P, P+N) of every
+ * cache hold a forest of draft nodes: parent[i] in [-1, i), -1 = a child of
+ * the last prefix token.  last = the deepest forest node on the newly
+ * verified path (-1: none).  path = the forest root ... last (L nodes, L = 0
+ * if last = -1); kept = the nodes below last in index order (S nodes; none
+ * unless keep).  Rows P + i take the old rows of (path ++ kept)[i]; other
+ * rows are unchanged.  new_parent[j] (j < S) = position in kept of kept[j]'s
+ * parent, or -1 if that parent is last.  Returns L (the prefix grows by L),
+ * *n_kept = S; -1 for invalid arguments or forest. */
+int32_t oracle_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers, int64_t layer_stride,
+                             int32_t Hkv, int32_t S_max, int32_t D, int32_t P, const int32_t* parent,
+                             int32_t N, int32_t last, int32_t keep, int32_t* new_parent, int32_t* n_kept);
+
 /* Greedy acceptance of a verified tree (target-side verification with the
  * target's greedy choice; Sec. 3.1, Fig. 3 walk-through).  logits [T][ldl]
  * fp16: row i is the target's distribution after the path root -> node i.

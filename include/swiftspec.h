@@ -223,6 +223,28 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
                         const int32_t* d_accepted_node, int32_t advance, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* Draft-side KV reorganisation after re-rooting (Sec. 3.2, consistency
+ * management of the draft model's cache; Fig. 5).  Rows [P, P+N) of each
+ * [Hkv][S_max][D] cache (layer l at k_cache + l * layer_stride_elems) hold
+ * the draft tree cache: a forest, d_parent[N] with parent[i] in [-1, i)
+ * (-1: a child of the last prefix token).  *d_last = the deepest forest node
+ * on the newly verified token sequence, or -1 if the first verified token
+ * is not in the forest.  Rows P .. P+L-1 take the verified path (the forest
+ * root above last, ..., last; L = 0 if last = -1); if *d_keep != 0 the nodes
+ * below last follow in index order (S of them, rows P+L .. P+L+S-1), else
+ * S = 0; all other rows are unchanged.  d_new_parent (nullable, N entries)
+ * receives, for j < S, the new tree-cache index of kept node j's parent, or
+ * -1 if that parent is last (now the last prefix token); *d_n_kept
+ * (nullable) = S.  If advance != 0, *d_prefix_len becomes P + L after the
+ * copy (stream-ordered).  With *d_keep == 0 and a single-root tree this is
+ * swiftspec_kv_commit.  1 <= N <= 64, D % 8 == 0, D <= 256, caches 16-byte
+ * aligned.  Invalid device data (forest, last, prefix) sets the error word
+ * (ws may be NULL: then it is not reported) and nothing is written. */
+int swiftspec_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers, int64_t layer_stride_elems,
+                            int32_t Hkv, int32_t S_max, int32_t D, int32_t* d_prefix_len, const int32_t* d_parent,
+                            int32_t N, const int32_t* d_last, const int32_t* d_keep, int32_t* d_new_parent,
+                            int32_t* d_n_kept, int32_t advance, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------- greedy acceptance
  * Closes a verification step on the device (Sec. 3.1, Fig. 3 walk-through:
  * an iteration's output is the accepted root path followed by one token

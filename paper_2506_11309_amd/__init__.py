@@ -58,6 +58,8 @@ _SIGS = {
     "swiftspec_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "swiftspec_last_hip_error": ([], ctypes.c_int),
     "swiftspec_workspace_init": ([vp, sz, vp], ctypes.c_int),
+    "swiftspec_kv_reorganize": ([vp, vp, i32, i64, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, i32, vp, sz, vp],
+                                ctypes.c_int),
     "swiftspec_greedy_accept_workspace_bytes": ([i32], sz),
     "swiftspec_greedy_accept": ([vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     "swiftspec_read_device_error": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
@@ -300,6 +302,21 @@ def kv_commit(k_cache, v_cache, prefix_len, parent, accepted, n_layers=1, layer_
                                      int(bool(advance)), _ptr(ws), ws.numel() if ws is not None else 0,
                                      _stream(stream))
     _check(st, "kv_commit")
+
+
+def kv_reorganize(k_cache, v_cache, prefix_len, parent, last, keep, new_parent=None, n_kept=None, n_layers=1,
+                  layer_stride=None, advance=False, ws=None, stream=None):
+    """Draft-side reorganisation on caches [n_layers][Hkv][S_max][D] (or
+    [Hkv][S_max][D]); prefix_len, parent [N], last, keep and the outputs
+    new_parent [N], n_kept are device int32 tensors."""
+    Hkv, S_max, D = k_cache.shape[-3:]
+    if layer_stride is None:
+        layer_stride = Hkv * S_max * D
+    st = _load().swiftspec_kv_reorganize(_ptr(k_cache), _ptr(v_cache), n_layers, layer_stride, Hkv, S_max, D,
+                                         _ptr(prefix_len), _ptr(parent), parent.shape[0], _ptr(last), _ptr(keep),
+                                         _ptr(new_parent), _ptr(n_kept), int(bool(advance)), _ptr(ws),
+                                         ws.numel() if ws is not None else 0, _stream(stream))
+    _check(st, "kv_reorganize")
 
 
 def greedy_accept_workspace_bytes(T) -> int:

@@ -162,6 +162,117 @@ void launch_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_
                        S_max);
 }
 
+// ------------------------------------------- draft-side KV reorganisation
+// The draft model's cache after re-rooting (Sec. 3.2, Fig. 5): rows
+// [P, P+N) hold a forest of draft nodes (parent -1: below the last prefix
+// token).  Wave 0 of every workgroup derives, from the forest's
+// ancestor-or-self masks, the verified path (the set bits of last's mask,
+// in increasing order: indices grow along any root path) and, if kept, the
+// nodes having `last` as a proper ancestor (in increasing order); row P + i
+// then takes the old row of the i-th node of path ++ kept, with the same
+// read-all-then-write pattern as the commit.  Workgroup 0 also writes the
+// kept nodes' parents renumbered into the new tree cache (-1 below last).
+__device__ __forceinline__ bool reorg_setup(const int32_t* parent, int N, const int32_t* d_last,
+                                            const int32_t* d_keep, const int32_t* prefix_len, int S_max,
+                                            int* s_rows, int* s_L, int* s_S, int* s_P, int* s_err,
+                                            int32_t* new_parent) {
+  // wave 0 only
+  uint64_t anc;
+  int depth;
+  const bool ok = tree_masks_wave<true>(parent, N, anc, depth);
+  const int lane = lane_id();
+  const int last = *d_last;
+  const bool keep = *d_keep != 0;
+  const int P = *prefix_len;
+  int err = 0;
+  if (!ok) err |= SWIFTSPEC_DEVERR_BAD_TREE;
+  if (last < -1 || last >= N) err |= SWIFTSPEC_DEVERR_BAD_ACCEPTED;
+  if (P < 0 || P > S_max - N) err |= SWIFTSPEC_DEVERR_BAD_PREFIX;
+  const bool have = err == 0 && last >= 0;
+  const uint64_t path = have ? shfl_u64(anc, last) : 0ull;
+  const bool mine_kept = have && keep && lane < N && lane != last && ((anc >> last) & 1ull);
+  const uint64_t kept = __ballot(mine_kept);
+  const int L = __popcll(path), S = __popcll(kept);
+  const uint64_t below = (1ull << lane) - 1ull;
+  if (lane < N && ((path >> lane) & 1ull)) s_rows[__popcll(path & below)] = lane;
+  if (mine_kept) {
+    const int j = __popcll(kept & below);
+    s_rows[L + j] = lane;
+    if (new_parent) {
+      const int p = parent[lane];
+      new_parent[j] = p == last ? -1 : __popcll(kept & ((1ull << p) - 1ull));
+    }
+  }
+  if (lane == 0) {
+    *s_L = L;
+    *s_S = S;
+    *s_P = P;
+    *s_err = err;
+  }
+  return err == 0;
+}
+
+__global__ __launch_bounds__(256) void kv_reorganize_kernel(uint16_t* k_cache, uint16_t* v_cache,
+                                                            int64_t layer_stride, int Hkv, int S_max, int D,
+                                                            const int32_t* prefix_len, const int32_t* parent,
+                                                            int N, const int32_t* d_last, const int32_t* d_keep,
+                                                            int32_t* new_parent, int32_t* n_kept, void* ws) {
+  __shared__ int s_rows[64];
+  __shared__ int s_L, s_S, s_P, s_err;
+  const int idx = blockIdx.x;
+  const int head = idx % Hkv;
+  const int which = (idx / Hkv) & 1;
+  const int layer = idx / (2 * Hkv);
+  if (threadIdx.x < 64)
+    reorg_setup(parent, N, d_last, d_keep, prefix_len, S_max, s_rows, &s_L, &s_S, &s_P, &s_err,
+                idx == 0 ? new_parent : nullptr);
+  __syncthreads();
+  if (s_err) {
+    if (idx == 0 && threadIdx.x == 0) report_error(ws, (uint32_t)s_err);
+    return;
+  }
+  const int R = s_L + s_S, P = s_P;
+  if (idx == 0 && threadIdx.x == 0 && n_kept) *n_kept = s_S;
+  uint16_t* base = (which ? v_cache : k_cache) + (size_t)layer * layer_stride + ((size_t)head * S_max + P) * D;
+  const int vec_per_row = D / 8;
+  const int rows_per_pass = 256 / vec_per_row;
+  const int c8 = (threadIdx.x % vec_per_row) * 8;
+  const int r0 = threadIdx.x / vec_per_row;
+  u32x4 buf[kCommitMaxRowsPerThread];
+#pragma unroll
+  for (int j = 0; j < kCommitMaxRowsPerThread; ++j) {
+    const int i = r0 + j * rows_per_pass;
+    if (i < R) buf[j] = *reinterpret_cast<const u32x4*>(base + (size_t)s_rows[i] * D + c8);
+  }
+  __syncthreads();  // every source row read before any row is written
+#pragma unroll
+  for (int j = 0; j < kCommitMaxRowsPerThread; ++j) {
+    const int i = r0 + j * rows_per_pass;
+    if (i < R) *reinterpret_cast<u32x4*>(base + (size_t)i * D + c8) = buf[j];
+  }
+}
+
+// The prefix grows by the path length (after the copy kernel, in stream order).
+__global__ void reorg_prefix_advance_kernel(int32_t* prefix_len, const int32_t* parent, int N, const int32_t* d_last,
+                                            const int32_t* d_keep, int S_max) {
+  __shared__ int s_rows[64];
+  __shared__ int s_L, s_S, s_P, s_err;
+  reorg_setup(parent, N, d_last, d_keep, prefix_len, S_max, s_rows, &s_L, &s_S, &s_P, &s_err, nullptr);
+  __syncthreads();
+  if (threadIdx.x == 0 && s_err == 0) *prefix_len = s_P + s_L;
+}
+
+void launch_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_t layer_stride, int Hkv,
+                          int S_max, int D, int32_t* prefix_len, const int32_t* parent, int N, const int32_t* d_last,
+                          const int32_t* d_keep, int32_t* new_parent, int32_t* n_kept, int advance, void* ws,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(kv_reorganize_kernel, dim3(n_layers * 2 * Hkv), dim3(256), 0, st, k_cache, v_cache,
+                     layer_stride, Hkv, S_max, D, prefix_len, parent, N, d_last, d_keep, new_parent, n_kept, ws);
+  if (advance)
+    hipLaunchKernelGGL(reorg_prefix_advance_kernel, dim3(1), dim3(64), 0, st, prefix_len, parent, N, d_last, d_keep,
+                       S_max);
+}
+
 // ---------------------------------------------------------- tree masks
 __global__ __launch_bounds__(64) void tree_masks_kernel(const int32_t* parents, int T, uint64_t* anc,
                                                         int32_t* depth, int32_t* status) {

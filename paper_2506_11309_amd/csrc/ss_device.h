@@ -45,12 +45,15 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
 // its root path, so 6 rounds cover any depth below 64.  Must be called by
 // all 64 lanes of a wave.  Returns false (for every lane) if the array is
 // not a valid increasing tree; then anc = own bit and depth = 0.
+// kForest: any node may be a root (parent -1), as in a draft model's tree
+// cache below its last prefix token; otherwise node 0 is the only root.
+template <bool kForest = false>
 __device__ __forceinline__ bool tree_masks_wave(const int32_t* __restrict__ parent, int T,
                                                 uint64_t& anc, int& depth) {
   const int lane = lane_id();
   int p = -1;
   if (lane < T) p = parent[lane];
-  bool ok = lane >= T || (lane == 0 ? p == -1 : (p >= 0 && p < lane));
+  bool ok = lane >= T || (kForest ? (p >= -1 && p < lane) : (lane == 0 ? p == -1 : (p >= 0 && p < lane)));
   const bool all_ok = __all(ok);
   uint64_t a = lane < T ? (1ull << lane) : 0ull;
   if (!all_ok) {

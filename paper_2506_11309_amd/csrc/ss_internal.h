@@ -91,6 +91,10 @@ void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc
 
 void launch_ws_init(void* ws, size_t bytes, hipStream_t st);
 
+void launch_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_t layer_stride, int Hkv,
+                          int S_max, int D, int32_t* prefix_len, const int32_t* parent, int N, const int32_t* d_last,
+                          const int32_t* d_keep, int32_t* new_parent, int32_t* n_kept, int advance, void* ws,
+                          hipStream_t st);
 int greedy_accept_splits(int T);  // workgroups per logits row
 void launch_greedy_accept(const uint16_t* logits, int ldl, int T, int V, const int32_t* tokens,
                           const int32_t* parent, int32_t* argmax, int32_t* accepted, int32_t* bonus,

@@ -454,6 +454,22 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
   return check_launch();
 }
 
+int swiftspec_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers, int64_t layer_stride_elems,
+                            int32_t Hkv, int32_t S_max, int32_t D, int32_t* d_prefix_len, const int32_t* d_parent,
+                            int32_t N, const int32_t* d_last, const int32_t* d_keep, int32_t* d_new_parent,
+                            int32_t* d_n_kept, int32_t advance, void* ws, size_t ws_bytes, void* stream) {
+  if (!k_cache || !v_cache || !d_prefix_len || !d_parent || !d_last || !d_keep) return SWIFTSPEC_INVALID_ARG;
+  if (n_layers < 1 || Hkv < 1 || N < 1 || S_max < N || D < 8) return SWIFTSPEC_INVALID_ARG;
+  if (layer_stride_elems < (int64_t)Hkv * S_max * D) return SWIFTSPEC_INVALID_ARG;
+  if (N > SWIFTSPEC_MAX_TREE || D % 8 || D > 256) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || layer_stride_elems % 8) return SWIFTSPEC_MISALIGNED;
+  if (ws && ws_bytes < kHeader) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  if ((int64_t)n_layers * 2 * Hkv > 0x7fffffff) return SWIFTSPEC_UNSUPPORTED;
+  ss::launch_kv_reorganize(k_cache, v_cache, n_layers, layer_stride_elems, Hkv, S_max, D, d_prefix_len, d_parent, N,
+                           d_last, d_keep, d_new_parent, d_n_kept, advance, ws, S(stream));
+  return check_launch();
+}
+
 size_t swiftspec_greedy_accept_workspace_bytes(int32_t T) {
   if (T < 1 || T > SWIFTSPEC_MAX_TREE) return kHeader;
   return kHeader + align_up((size_t)T * ss::greedy_accept_splits(T) * 8);

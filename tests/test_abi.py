@@ -92,6 +92,14 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert acc(8, 1000, 1000, ws=None) == ss.INVALID_ARG
     assert acc(8, 1000, 1000, bonus=None) == ss.INVALID_ARG
     assert lib.swiftspec_greedy_accept_workspace_bytes(64) >= ss.WS_HEADER_BYTES + 64 * 16 * 8
+    # draft-side reorganisation: forest size, head dim, layer stride, nulls
+    reorg = lambda N, D=128, stride=8 * 200 * 128, last=fake: lib.swiftspec_kv_reorganize(
+        fake, fake, 2, stride, 8, 200, D, fake, fake, N, last, fake, None, None, 0, None, 0, None)
+    assert reorg(0) == ss.INVALID_ARG
+    assert reorg(65) == ss.UNSUPPORTED
+    assert reorg(8, D=100) == ss.UNSUPPORTED
+    assert reorg(8, stride=100) == ss.INVALID_ARG
+    assert reorg(8, last=None) == ss.INVALID_ARG
 
 
 def test_verify_step_rejects_before_launch(ss):

@@ -64,6 +64,9 @@ def _load():
     lib.oracle_verify_layer.restype = ctypes.c_int
     lib.oracle_lm_head.argtypes = [vp, i32, i32, vp, dbl, vp, i32, vp]
     lib.oracle_lm_head.restype = ctypes.c_int
+    lib.oracle_draft_tree_attention.argtypes = [vp, i32, vp, vp, i32, vp, vp, i32, i32, vp, i32, vp, i32, i32,
+                                                i32, i32, dbl, dbl, vp, i32]
+    lib.oracle_draft_tree_attention.restype = ctypes.c_int
     lib.oracle_kv_reorganize.argtypes = [vp, vp, i32, i64, i32, i32, i32, i32, vp, i32, i32, i32, vp, vp]
     lib.oracle_kv_reorganize.restype = i32
     lib.oracle_greedy_accept.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
@@ -186,6 +189,27 @@ def tree_attention(q, k, v, k_cache, v_cache, P, parent, Hq, Hkv, D, rope_theta=
                                        softmax_scale, _p(out), Hq * D)
     if rc != 0:
         raise ValueError("oracle_tree_attention: invalid arguments or tree")
+    return out
+
+
+def draft_tree_attention(q, k, v, k_cache, v_cache, P, cache_parent, leaf_parent, Hq, Hkv, D,
+                         rope_theta=500000.0, softmax_scale=None):
+    """Draft-model attention with the non-square mask; caches [Hkv][S_max][D]
+    updated in place (rows P + N + i); returns out [w][Hq*D]."""
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    cp = _c(cache_parent, np.int32) if len(cache_parent) else np.zeros(1, np.int32)
+    lp = _c(leaf_parent, np.int32)
+    w = q.shape[0]
+    assert len(lp) == w and k_cache.flags["C_CONTIGUOUS"] and v_cache.flags["C_CONTIGUOUS"]
+    S_max = k_cache.shape[1]
+    if softmax_scale is None:
+        softmax_scale = 1.0 / np.sqrt(D)
+    out = np.empty((w, Hq * D), np.uint16)
+    rc = _load().oracle_draft_tree_attention(_p(q), q.shape[1], _p(k), _p(v), k.shape[1], _p(k_cache), _p(v_cache),
+                                             S_max, P, _p(cp), len(cache_parent), _p(lp), w, Hq, Hkv, D, rope_theta,
+                                             softmax_scale, _p(out), Hq * D)
+    if rc != 0:
+        raise ValueError("oracle_draft_tree_attention: invalid arguments or forest")
     return out
 
 

@@ -283,6 +283,88 @@ int oracle_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, con
   return 0;
 }
 
+/* Draft-model attention with a non-square mask (Sec. 3.1, Fig. 4). */
+int oracle_draft_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                                int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max, int32_t P,
+                                const int32_t* cache_parent, int32_t N, const int32_t* leaf_parent, int32_t w,
+                                int32_t Hq, int32_t Hkv, int32_t D, double rope_theta, double softmax_scale,
+                                uint16_t* out, int32_t ldo) {
+  if (w < 1 || N < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv || D < 2 || D % 2 || D > 1024 || P < 0 ||
+      P + N + w > S_max)
+    return -1;
+  if (ldq < Hq * D || ldkv < Hkv * D || ldo < Hq * D) return -1;
+  for (int32_t j = 0; j < N; ++j)
+    if (cache_parent[j] < -1 || cache_parent[j] >= j) return -1;
+  for (int32_t i = 0; i < w; ++i)
+    if (leaf_parent[i] < -1 || leaf_parent[i] >= N) return -1;
+  /* depth of each cached node (a node below the last prefix token has depth
+     0, at position P) and of each new token (one more than its parent's) */
+  int32_t* cdepth = (int32_t*)malloc(sizeof(int32_t) * (N > 0 ? N : 1));
+  for (int32_t j = 0; j < N; ++j) {
+    int32_t d = 0;
+    for (int32_t u = cache_parent[j]; u != -1; u = cache_parent[u]) d++;
+    cdepth[j] = d;
+  }
+  int32_t* pos = (int32_t*)malloc(sizeof(int32_t) * w);
+  for (int32_t i = 0; i < w; ++i) pos[i] = P + (leaf_parent[i] < 0 ? 0 : cdepth[leaf_parent[i]] + 1);
+  /* visibility: new token i sees the prefix, the cached nodes on its
+     parent's root path (the parent included) and itself */
+  uint8_t* vis_cache = (uint8_t*)calloc((size_t)w * (N > 0 ? N : 1), 1);
+  for (int32_t i = 0; i < w; ++i)
+    for (int32_t u = leaf_parent[i]; u != -1; u = cache_parent[u]) vis_cache[(size_t)i * N + u] = 1;
+  /* 1. the new keys and values enter the cache at rows P + N + i */
+  for (int32_t g = 0; g < Hkv; ++g)
+    for (int32_t i = 0; i < w; ++i) {
+      double kv[1024];
+      for (int32_t d = 0; d < D; ++d) kv[d] = oracle_f16_to_f64(k[(size_t)i * ldkv + g * D + d]);
+      oracle_rope(kv, D, (int64_t)pos[i], rope_theta);
+      size_t row = ((size_t)g * S_max + P + N + i) * D;
+      for (int32_t d = 0; d < D; ++d) {
+        k_cache[row + d] = oracle_f64_to_f16(kv[d]);
+        v_cache[row + d] = v[(size_t)i * ldkv + g * D + d];
+      }
+    }
+  /* 2. masked softmax attention per (head, new token) */
+  const int32_t group = Hq / Hkv;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int32_t h = 0; h < Hq; ++h)
+    for (int32_t i = 0; i < w; ++i) {
+      const int32_t g = h / group;
+      double qr[1024];
+      for (int32_t d = 0; d < D; ++d) qr[d] = oracle_f16_to_f64(q[(size_t)i * ldq + h * D + d]);
+      oracle_rope(qr, D, (int64_t)pos[i], rope_theta);
+      const int32_t nkeys = P + N + w;
+      double* sc = (double*)malloc(sizeof(double) * nkeys);
+      char* vis = (char*)malloc(nkeys);
+      double mx = -INFINITY;
+      for (int32_t r = 0; r < nkeys; ++r) {
+        vis[r] = r < P ? 1 : r < P + N ? vis_cache[(size_t)i * N + (r - P)] : (r == P + N + i);
+        if (!vis[r]) continue;
+        const uint16_t* kr = k_cache + ((size_t)g * S_max + r) * D;
+        double dot = 0.0;
+        for (int32_t d = 0; d < D; ++d) dot += qr[d] * oracle_f16_to_f64(kr[d]);
+        sc[r] = dot * softmax_scale;
+        if (sc[r] > mx) mx = sc[r];
+      }
+      double l = 0.0, o[1024];
+      for (int32_t d = 0; d < D; ++d) o[d] = 0.0;
+      for (int32_t r = 0; r < nkeys; ++r) {
+        if (!vis[r]) continue;
+        const double p = exp(sc[r] - mx);
+        l += p;
+        const uint16_t* vr = v_cache + ((size_t)g * S_max + r) * D;
+        for (int32_t d = 0; d < D; ++d) o[d] += p * oracle_f16_to_f64(vr[d]);
+      }
+      for (int32_t d = 0; d < D; ++d) out[(size_t)i * ldo + h * D + d] = oracle_f64_to_f16(o[d] / l);
+      free(sc);
+      free(vis);
+    }
+  free(cdepth);
+  free(pos);
+  free(vis_cache);
+  return 0;
+}
+
 /* ------------------------------------------------------------------ commit */
 
 int32_t oracle_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,

@@ -88,6 +88,24 @@ int32_t oracle_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
                          int64_t layer_stride, int32_t Hkv, int32_t S_max, int32_t D, int32_t P,
                          const int32_t* parent, int32_t T, int32_t accepted);
 
+/* Draft-model attention with a non-square mask (Sec. 3.1, paragraph on
+ * non-square masks; Fig. 4): the draft model expands w leaves of its tree.
+ * Cache rows [0, P) hold the verified prefix, rows [P, P+N) the draft tree
+ * cache (a forest: cache_parent[j] in [-1, j), -1 = below the last prefix
+ * token), all already rotated.  New token i (a leaf below cache node
+ * leaf_parent[i], -1 = below the last prefix token) sits at position
+ * P + depth, where a cached node below the last prefix token has depth 0
+ * and a new token one more than its parent (so position P if its parent is
+ * -1).  Its key, rotated at that position and rounded to fp16, and its
+ * value enter rows P + N + i.  It attends to the whole prefix, to the cached
+ * nodes on its parent's root path (parent included) and to itself: a
+ * w x (N + w) mask over the tree region.  Returns 0 or -1. */
+int oracle_draft_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                                int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max, int32_t P,
+                                const int32_t* cache_parent, int32_t N, const int32_t* leaf_parent, int32_t w,
+                                int32_t Hq, int32_t Hkv, int32_t D, double rope_theta, double softmax_scale,
+                                uint16_t* out, int32_t ldo);
+
 /* Draft-side KV reorganisation after re-rooting (Sec. 3.2, consistency
  * management of the draft model's cache; Fig. 5).  Rows [P, P+N) of every
  * cache hold a forest of draft nodes: parent[i] in [-1, i), -1 = a child of

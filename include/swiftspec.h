@@ -223,6 +223,31 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
                         const int32_t* d_accepted_node, int32_t advance, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* Draft-model tree attention with a non-square mask (Sec. 3.1, paragraph
+ * on non-square masks; Fig. 4): the draft model expands w leaves of its
+ * tree.  Cache rows [0, P) hold the verified prefix (P = *d_prefix_len),
+ * rows [P, P+N) the draft tree cache, already rotated: a forest,
+ * d_cache_parent[N] with parent[j] in [-1, j) (-1: below the last prefix
+ * token).  New token i (q, k, v rows i, layouts as in
+ * swiftspec_tree_attention, k pre-rotation) is a leaf below cache node
+ * d_leaf_parent[i] (-1: below the last prefix token) at position P + depth
+ * (a cached node below the last prefix token has depth 0, a new token one
+ * more than its parent).  Its rotated key (fp16) and its value are written
+ * to rows P + N + i, and it attends to the whole prefix, to the cached
+ * nodes on its parent's root path (parent included) and to itself: a
+ * w x (N + w) mask over the tree region.  1 <= w <= 64, 0 <= N <= 64,
+ * P + N + w <= S_max (else the device error word gets
+ * SWIFTSPEC_DEVERR_BAD_PREFIX), other requirements and the workspace
+ * (swiftspec_tree_attention_workspace_bytes(w, Hq, Hkv, D, S_max)) as for
+ * swiftspec_tree_attention.  An invalid forest or leaf parent sets
+ * SWIFTSPEC_DEVERR_BAD_TREE and leaves output and cache untouched. */
+int swiftspec_draft_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                                   int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
+                                   const int32_t* d_prefix_len, const int32_t* d_cache_parent, int32_t N,
+                                   const int32_t* d_leaf_parent, int32_t w, int32_t Hq, int32_t Hkv, int32_t D,
+                                   const float* rope_cos_sin, float softmax_scale, uint16_t* out, int32_t ldo,
+                                   void* ws, size_t ws_bytes, void* stream);
+
 /* Draft-side KV reorganisation after re-rooting (Sec. 3.2, consistency
  * management of the draft model's cache; Fig. 5).  Rows [P, P+N) of each
  * [Hkv][S_max][D] cache (layer l at k_cache + l * layer_stride_elems) hold

@@ -58,6 +58,8 @@ _SIGS = {
     "swiftspec_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "swiftspec_last_hip_error": ([], ctypes.c_int),
     "swiftspec_workspace_init": ([vp, sz, vp], ctypes.c_int),
+    "swiftspec_draft_tree_attention": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, i32, vp, i32, i32, i32, i32, vp,
+                                        f32, vp, i32, vp, sz, vp], ctypes.c_int),
     "swiftspec_kv_reorganize": ([vp, vp, i32, i64, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, i32, vp, sz, vp],
                                 ctypes.c_int),
     "swiftspec_greedy_accept_workspace_bytes": ([i32], sz),
@@ -302,6 +304,24 @@ def kv_commit(k_cache, v_cache, prefix_len, parent, accepted, n_layers=1, layer_
                                      int(bool(advance)), _ptr(ws), ws.numel() if ws is not None else 0,
                                      _stream(stream))
     _check(st, "kv_commit")
+
+
+def draft_tree_attention(q, k, v, k_cache, v_cache, prefix_len, cache_parent, leaf_parent, Hq, Hkv, rope, out, ws,
+                         softmax_scale=None, stream=None):
+    """Draft-model attention with the non-square mask: q [w][>=Hq*D],
+    k / v [w][>=Hkv*D] (strided views allowed), caches [Hkv][S_max][D],
+    cache_parent [N] (None or empty for N = 0) and leaf_parent [w] device
+    int32."""
+    Hkv_, S_max, D = k_cache.shape
+    w = q.shape[0]
+    N = 0 if cache_parent is None else cache_parent.shape[0]
+    scale = softmax_scale if softmax_scale is not None else 1.0 / (D ** 0.5)
+    st = _load().swiftspec_draft_tree_attention(_ptr(q), q.stride(0), _ptr(k), _ptr(v), k.stride(0), _ptr(k_cache),
+                                                _ptr(v_cache), S_max, _ptr(prefix_len),
+                                                _ptr(cache_parent) if N else None, N, _ptr(leaf_parent), w, Hq, Hkv,
+                                                D, _ptr(rope), scale, _ptr(out), out.stride(0), _ptr(ws), ws.numel(),
+                                                _stream(stream))
+    _check(st, "draft_tree_attention")
 
 
 def kv_reorganize(k_cache, v_cache, prefix_len, parent, last, keep, new_parent=None, n_kept=None, n_layers=1,

@@ -62,6 +62,11 @@ struct AttnLaunch {
   const int32_t* prefix_len;
   const int32_t* parent;
   int T, Hq, Hkv, D;
+  // draft model: N tree-cache rows after the prefix (forest cache_parent),
+  // the T new tokens are leaves below leaf_parent[i]; target: 0, NULL, NULL
+  int N = 0;
+  const int32_t* cache_parent = nullptr;
+  const int32_t* leaf_parent = nullptr;
   const float* rope;
   float scale;
   uint16_t* out;

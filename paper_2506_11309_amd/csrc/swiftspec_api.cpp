@@ -126,9 +126,13 @@ size_t attn_ws(int T, int Hq, int Hkv, int D, int S_max) {
 void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v, int ldkv,
                    uint16_t* kc, uint16_t* vc, int S_max, const int32_t* P, const int32_t* parent,
                    int T, int Hq, int Hkv, int D, const float* rope, float scale, uint16_t* out,
-                   int ldo, uint16_t* out_prep, void* ws, float* part, hipStream_t st) {
+                   int ldo, uint16_t* out_prep, void* ws, float* part, hipStream_t st, int N = 0,
+                   const int32_t* cache_parent = nullptr, const int32_t* leaf_parent = nullptr) {
   ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max);
   ss::AttnLaunch L;
+  L.N = N;
+  L.cache_parent = cache_parent;
+  L.leaf_parent = leaf_parent;
   L.q = q;
   L.ldq = ldq;
   L.k = k;
@@ -451,6 +455,29 @@ int swiftspec_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers,
   if ((int64_t)n_layers * 2 * Hkv > 0x7fffffff) return SWIFTSPEC_UNSUPPORTED;
   ss::launch_kv_commit(k_cache, v_cache, n_layers, layer_stride_elems, Hkv, S_max, D, d_prefix_len,
                        d_parent, T, d_accepted_node, advance, ws, S(stream));
+  return check_launch();
+}
+
+int swiftspec_draft_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                                   int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
+                                   const int32_t* d_prefix_len, const int32_t* d_cache_parent, int32_t N,
+                                   const int32_t* d_leaf_parent, int32_t w, int32_t Hq, int32_t Hkv, int32_t D,
+                                   const float* rope_cos_sin, float softmax_scale, uint16_t* out, int32_t ldo,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  if (N < 0 || (N > 0 && !d_cache_parent) || !d_leaf_parent) return SWIFTSPEC_INVALID_ARG;
+  if (N > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_UNSUPPORTED;
+  if ((int64_t)N + w > S_max) return SWIFTSPEC_INVALID_ARG;
+  // the same checks as the target attention over w new tokens (d_leaf_parent
+  // stands in for the parent array)
+  int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_leaf_parent, w,
+                                     Hq, Hkv, D, rope_cos_sin, out, ldo);
+  if (rc) return rc;
+  if (!ws) return SWIFTSPEC_INVALID_ARG;
+  if (ws_bytes < attn_ws(w, Hq, Hkv, D, S_max)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  run_attention(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_leaf_parent, w, Hq, Hkv, D,
+                rope_cos_sin, softmax_scale, out, ldo, nullptr, ws,
+                reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream), N, d_cache_parent,
+                d_leaf_parent);
   return check_launch();
 }
 

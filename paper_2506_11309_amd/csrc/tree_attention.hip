@@ -51,6 +51,13 @@ struct AttnArgs {
   float* part;
   int ldq, ldkv, ldo, S_max, T, Hq, Hkv, G, R, RB, nsplit;
   float scale_log2;  // softmax scale * log2(e)
+  // draft model (non-square mask): N tree-cache rows [P, P+N) below the
+  // prefix (a forest, cache_parent), the T new tokens are leaves below
+  // leaf_parent[i] and see only themselves among the new rows; target
+  // model: N = 0, leaf_parent = NULL, the T new tokens form the tree
+  int N;
+  const int32_t* cache_parent;
+  const int32_t* leaf_parent;
 };
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -98,6 +105,7 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
   __shared__ uint16_t ks[kAttnLds][kKeyTile * KST];
   __shared__ uint16_t vs[kAttnLds][kKeyTile * KST];
   __shared__ uint64_t s_anc[64];
+  __shared__ uint64_t s_cmask[64];  // draft model: visible tree-cache rows of each new token
   __shared__ int32_t s_depth[64];
   __shared__ int32_t s_status;
 
@@ -115,14 +123,15 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
   // ---- prefix length; this split's first key tiles go out before anything
   // else (an out-of-range P addresses from 0 and is rejected below) ----
   const int P_dev = __builtin_amdgcn_readfirstlane(*a.prefix_len);
-  const bool p_ok = P_dev >= 0 && P_dev <= a.S_max - a.T;
+  const bool p_ok = P_dev >= 0 && P_dev <= a.S_max - a.T - a.N;
   const int P = p_ok ? P_dev : 0;
+  const int PK = P + a.N;  // the splits stream keys [0, PK); the new rows go to PK + i
   int k_lo = 0, k_hi = 0, ntiles = 0;
   if (!tree_split) {
-    const int per = (P + a.nsplit - 1) / a.nsplit;
+    const int per = (PK + a.nsplit - 1) / a.nsplit;
     const int chunk = ((per + kKeyTile - 1) / kKeyTile) * kKeyTile;
-    k_lo = min(P, sp * chunk);
-    k_hi = min(P, k_lo + chunk);
+    k_lo = min(PK, sp * chunk);
+    k_hi = min(PK, k_lo + chunk);
     ntiles = (k_hi - k_lo + kKeyTile - 1) / kKeyTile;
   }
   k_lo = __builtin_amdgcn_readfirstlane(k_lo);
@@ -157,10 +166,31 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
 
   // ---- tree masks and validity ----
   if (wave == 0) {
-    uint64_t anc;
+    uint64_t anc, cmask = 0ull;
     int depth;
-    const bool ok = tree_masks_wave(a.parent, a.T, anc, depth);
+    bool ok;
+    if (a.leaf_parent) {
+      // draft model: the tree cache's forest masks; new token i sees the
+      // cached root path of its parent (the parent included) and itself,
+      // at depth one more than its parent's (0 below the last prefix token)
+      uint64_t canc;
+      int cdepth;
+      const bool fok = tree_masks_wave<true>(a.cache_parent, a.N, canc, cdepth);
+      const int lp = lane < a.T ? a.leaf_parent[lane] : -1;
+      const bool lok = __all(lane >= a.T || (lp >= -1 && lp < a.N));
+      const int src = (lp >= 0 && lp < a.N) ? lp : 0;
+      const uint64_t pm = shfl_u64(canc, src);
+      const int pd = __shfl(cdepth, src, kWave);
+      const bool has = lane < a.T && lp >= 0 && lp < a.N;
+      cmask = has ? pm : 0ull;
+      depth = has ? pd + 1 : 0;
+      anc = lane < a.T ? (1ull << lane) : 0ull;
+      ok = fok && lok;
+    } else {
+      ok = tree_masks_wave(a.parent, a.T, anc, depth);
+    }
     s_anc[lane] = anc;
+    s_cmask[lane] = cmask;
     s_depth[lane] = depth;
     if (lane == 0) {
       int st = 0;
@@ -230,9 +260,13 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   const uint64_t anc = s_anc[node];
+  const uint64_t cmask = s_cmask[node];
 
   // ---- one 64-key tile from LDS slot `slot`: scores, mask, softmax, P.V ----
-  auto compute = [&](int slot, int key_end, bool masked) {
+  // mode 0: no mask beyond key_end; 1: tree keys, ancestor-or-self bits;
+  // 2: streamed keys reaching the draft tree cache, key kr of the tile is
+  // row kbase + kr of the tree cache (negative: a prefix row)
+  auto compute = [&](int slot, int key_end, int mode, int kbase) {
     f32x4 s[4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
@@ -249,7 +283,7 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
     // the exponent, 2^(c s - m); full prefix tiles need no mask
     const float c2 = a.scale_log2;
     float tmax = -INFINITY;
-    if (!masked && key_end >= kKeyTile) {
+    if (mode == 0 && key_end >= kKeyTile) {
 #pragma unroll
       for (int st = 0; st < 4; ++st)
 #pragma unroll
@@ -261,7 +295,11 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
         for (int r = 0; r < 4; ++r) {
           const int kr = st * 16 + 4 * kq + r;
           bool ok = kr < key_end;
-          if (masked) ok = ok && ((anc >> kr) & 1ull);
+          if (mode == 1) ok = ok && ((anc >> kr) & 1ull);
+          if (mode == 2) {
+            const int cr = kbase + kr;
+            ok = ok && (cr < 0 || (cr < 64 && ((cmask >> (cr & 63)) & 1ull)));
+          }
           const float v = ok ? s[st][r] : -INFINITY;
           s[st][r] = v;
           tmax = fmaxf(tmax, v);
@@ -347,8 +385,8 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
         k1 = bitcast<u32x4>(o1);
         k2 = bitcast<u32x4>(o2);
         if (rb == 0) {
-          uint16_t* kd = a.k_cache + ((size_t)g * a.S_max + P + kr) * D;
-          uint16_t* vd = a.v_cache + ((size_t)g * a.S_max + P + kr) * D;
+          uint16_t* kd = a.k_cache + ((size_t)g * a.S_max + PK + kr) * D;
+          uint16_t* vd = a.v_cache + ((size_t)g * a.S_max + PK + kr) * D;
           *reinterpret_cast<u32x4*>(kd + c8) = k1;
           *reinterpret_cast<u32x4*>(kd + c8 + HALF) = k2;
           *reinterpret_cast<u32x4*>(vd + c8) = v1;
@@ -361,7 +399,7 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
       *reinterpret_cast<u32x4*>(&vs[0][kr * KST + c8 + HALF]) = v2;
     }
     __syncthreads();
-    compute(0, a.T, true);
+    compute(0, a.T, 1, 0);
   } else {
     // ---- prefix chunk of this split (first tiles already in flight) ----
     if (ntiles > 0) {
@@ -386,7 +424,8 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
           if (t < ntiles) {
             if (t + 1 < ntiles) store_tile((t + 1) % kAttnLds, kbuf[(J + 1) % kAttnRing], vbuf[(J + 1) % kAttnRing]);
             lds_barrier();
-            compute(t % kAttnLds, k_hi - (k_lo + t * kKeyTile), false);
+            const int key0 = k_lo + t * kKeyTile;
+            compute(t % kAttnLds, k_hi - key0, (a.N > 0 && key0 + kKeyTile > P) ? 2 : 0, key0 - P);
           } else {
             retire(kbuf[J], vbuf[J]);
           }
@@ -498,6 +537,9 @@ void launch_tree_attention(const AttnLaunch& L, hipStream_t st) {
   a.v_cache = L.v_cache;
   a.prefix_len = L.prefix_len;
   a.parent = L.parent;
+  a.N = L.N;
+  a.cache_parent = L.cache_parent;
+  a.leaf_parent = L.leaf_parent;
   a.rope = L.rope;
   a.out = L.out;
   a.out_prep = L.out_prep;

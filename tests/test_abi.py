@@ -92,6 +92,13 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert acc(8, 1000, 1000, ws=None) == ss.INVALID_ARG
     assert acc(8, 1000, 1000, bonus=None) == ss.INVALID_ARG
     assert lib.swiftspec_greedy_accept_workspace_bytes(64) >= ss.WS_HEADER_BYTES + 64 * 16 * 8
+    # draft attention: tree-cache size, missing forest, leaf count
+    dargs = lambda N, w=8, cp=fake: (fake, 2048, fake, fake, 512, fake, fake, 4096, fake, cp, N, fake, w, 32, 8, 64,
+                                     fake, ctypes.c_float(0.125), fake, 2048, fake, 1 << 30, None)
+    assert lib.swiftspec_draft_tree_attention(*dargs(65)) == ss.UNSUPPORTED
+    assert lib.swiftspec_draft_tree_attention(*dargs(4, cp=None)) == ss.INVALID_ARG
+    assert lib.swiftspec_draft_tree_attention(*dargs(4, w=65)) == ss.UNSUPPORTED
+    assert lib.swiftspec_draft_tree_attention(*dargs(-1)) == ss.INVALID_ARG
     # draft-side reorganisation: forest size, head dim, layer stride, nulls
     reorg = lambda N, D=128, stride=8 * 200 * 128, last=fake: lib.swiftspec_kv_reorganize(
         fake, fake, 2, stride, 8, 200, D, fake, fake, N, last, fake, None, None, 0, None, 0, None)

@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-full-step", action="store_true",
                     help="skip the 80-layer step (all layers + final norm + LM head) timing")
     ap.add_argument("--full-step-reps", type=int, default=10)
+    ap.add_argument("--no-draft-side", action="store_true",
+                    help="skip the draft-model kernels (non-square attention, KV reorganisation)")
     ap.add_argument("--gemm-ab", action="store_true",
                     help="only compare the matrix-core and vector-ALU W4A16 GEMMs over M (JSON line per M)")
     return ap.parse_args()
@@ -257,6 +259,7 @@ def main():
     traffic = read_traffic("swiglu_gemm_c3", source_hash(GEMM_SOURCES))
 
     full = None if args.no_full_step else full_step(args, ss, torch, np, dev, stream)
+    draft = None if args.no_draft_side else draft_side(args, ss, torch, np, dev, stream)
 
     # ---------------- CPU baseline: the fp64 reference checker ----------------
     cpu = None
@@ -305,9 +308,76 @@ def main():
                      "algorithmic_bytes_per_launch": sw_bytes, "avg_launch_us": round(sw_us, 3)},
         "cpu_baseline": cpu,
         "full_step_80_layers": full,
+        "draft_side": draft,
         "input_generation_s": round(gen_s, 2),
     }
     print(json.dumps(out), flush=True)
+
+
+def draft_side(args, ss, torch, np, dev, stream):
+    """The draft model's kernels at a Llama-3.2-1B-shaped draft (16 layers,
+    Hq/Hkv = 32/8, D = 64) next to the 70B target's prefix (P = 4096): one
+    tree expansion of w = 8 leaves over a 56-node tree cache (non-square
+    attention, one layer), and the KV reorganisation of all 16 layers after
+    re-rooting (path of 3 into the prefix, the subtree below it compacted).
+    Inputs seeded, timed as graphs of 20 launches replayed 20 times."""
+    from gen import device as gdev
+    from gen import workloads as wl
+    s = wl.LLAMA_1B
+    n_layers, P, N, w = 16, 4096, 56, 8
+    S_max = P + 64 + w
+    rng = np.random.default_rng(2506)
+    # forest: a chain of 3 from the prefix, the rest hung on random earlier nodes
+    cp = [-1, 0, 1] + [int(rng.integers(0, j)) for j in range(3, N)]
+    lp = [int(rng.integers(0, N)) for _ in range(w)]
+    dcp = torch.tensor(cp, dtype=torch.int32, device=dev)
+    dlp = torch.tensor(lp, dtype=torch.int32, device=dev)
+    dP = torch.tensor([P], dtype=torch.int32, device=dev)
+    kc = gdev.normal_f16_device(7, 0, (n_layers, s.Hkv, S_max, s.D), device=dev)
+    vc = gdev.normal_f16_device(7, 1, (n_layers, s.Hkv, S_max, s.D), device=dev)
+    q = gdev.normal_f16_device(7, 2, (w, s.Hq * s.D), device=dev)
+    k = gdev.normal_f16_device(7, 3, (w, s.Hkv * s.D), device=dev)
+    v = gdev.normal_f16_device(7, 4, (w, s.Hkv * s.D), device=dev)
+    out = torch.zeros((w, s.Hq * s.D), dtype=torch.int16, device=dev)
+    rope = torch.from_numpy(ss.rope_table(500000.0, S_max, s.D)).to(dev)
+    ws = ss.workspace(ss.tree_attention_workspace_bytes(w, s.Hq, s.Hkv, s.D, S_max), dev)
+    last = torch.tensor([2], dtype=torch.int32, device=dev)
+    keep = torch.tensor([1], dtype=torch.int32, device=dev)
+    newp = torch.zeros(N, dtype=torch.int32, device=dev)
+    nk = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def timed(enqueue, reps=20, inner=20):
+        g = ss.Graph()
+        with torch.cuda.stream(stream):
+            g.begin(stream)
+            for _ in range(inner):
+                enqueue()
+            g.end(stream)
+            g.launch(stream)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            ev[0].record(stream)
+            for i in range(reps):
+                g.launch(stream)
+                ev[i + 1].record(stream)
+        ev[-1].synchronize()
+        t = sorted(ev[i].elapsed_time(ev[i + 1]) / inner for i in range(reps))
+        return t[len(t) // 2] * 1000.0
+
+    attn_us = timed(lambda: ss.draft_tree_attention(q, k, v, kc[0], vc[0], dP, dcp, dlp, s.Hq, s.Hkv, rope, out, ws,
+                                                    stream=stream))
+    reorg_us = timed(lambda: ss.kv_reorganize(kc, vc, dP, dcp, last, keep, new_parent=newp, n_kept=nk,
+                                              n_layers=n_layers, advance=False, ws=ws, stream=stream))
+    if ss.read_device_error(ws, stream):
+        raise RuntimeError("device error in the draft-side kernels")
+    kept = int(nk.item())
+    attn_bytes = 2 * s.Hkv * (P + N + w) * s.D * 2   # K and V rows read (upper bound: every tree row)
+    reorg_bytes = n_layers * 2 * s.Hkv * (3 + kept) * s.D * 2 * 2
+    return {"workload": f"Llama-3.2-1B-shaped draft ({n_layers} layers, Hq/Hkv={s.Hq}/{s.Hkv}, D={s.D}); "
+                        f"prefix P={P}, tree cache N={N}, w={w} leaves expanded; re-rooting path 3, subtree {kept}",
+            "draft_attention_us": round(attn_us, 2),
+            "draft_attention_gbs": round(attn_bytes / (attn_us * 1e-6) / 1e9, 1),
+            "kv_reorganize_all_layers_us": round(reorg_us, 2),
+            "kv_reorganize_bytes": reorg_bytes}
 
 
 def full_step(args, ss, torch, np, dev, stream):

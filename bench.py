@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-full-step", action="store_true",
                     help="skip the 80-layer step (all layers + final norm + LM head) timing")
     ap.add_argument("--full-step-reps", type=int, default=10)
+    ap.add_argument("--no-paper-shard", action="store_true",
+                    help="skip the one-GPU share of the paper's 70B TP4 kernel benchmarks")
     ap.add_argument("--no-draft-side", action="store_true",
                     help="skip the draft-model kernels (non-square attention, KV reorganisation)")
     ap.add_argument("--gemm-ab", action="store_true",
@@ -260,6 +262,7 @@ def main():
 
     full = None if args.no_full_step else full_step(args, ss, torch, np, dev, stream)
     draft = None if args.no_draft_side else draft_side(args, ss, torch, np, dev, stream)
+    shard = None if args.no_paper_shard else paper_shard(args, ss, torch, np, dev, stream)
 
     # ---------------- CPU baseline: the fp64 reference checker ----------------
     cpu = None
@@ -309,9 +312,115 @@ def main():
         "cpu_baseline": cpu,
         "full_step_80_layers": full,
         "draft_side": draft,
+        "paper_tp4_shard": shard,
         "input_generation_s": round(gen_s, 2),
     }
     print(json.dumps(out), flush=True)
+
+
+def paper_shard(args, ss, torch, np, dev, stream):
+    """One GPU's share of the paper's own kernel benchmarks: Llama-3-70B
+    under tensor parallelism 4 at batch 8 (the per-operation table of Sec.
+    2.4 and the kernel table of Sec. 5.4, both measured on H800): QKV
+    K = 8192, N = 2560 (16 query and 2 KV heads); O K = 2048, N = 8192 (+
+    residual); SwiGLU K = 8192, N = 7168; down K = 7168, N = 8192 (+
+    residual); attention over 16 query / 2 KV heads, a tree of 8 tokens, at
+    the prefix lengths 500, 1000 and 4096.  The all-reduce is not measured
+    (one GPU).  Weights rotate over copies totalling >= 512 MB per
+    operation; graphs of 50 launches replayed 3 times.  `paper_us` is the
+    paper's number for the same operation (its own kernels, H800, BF16
+    compute), `speedup` = paper_us / us."""
+    from gen import device as gdev
+    M, H, Hq, Hkv, D = 8, 8192, 16, 2, 128
+    F = 28672 // 4
+    shapes = {"qkv": (H, (Hq + 2 * Hkv) * D, False), "o_proj": (Hq * D, H, True), "swiglu": (H, F, False),
+              "down": (F, H, True)}
+    paper = {"qkv": 16.9, "o_proj": 10.8, "swiglu": 39.3, "down": 18.1}
+
+    def timed(fn, iters=50):
+        g = ss.Graph()
+        with torch.cuda.stream(stream):
+            for i in range(2):
+                fn(i)
+            g.begin(stream)
+            for i in range(iters):
+                fn(i)
+            g.end(stream)
+            g.launch(stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                g.launch(stream)
+            e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1000.0 / (3 * iters)
+
+    x = torch.randint(-3000, 3000, (M, max(H, F)), dtype=torch.int16, device=dev) & 0x3BFF
+    y = torch.zeros((M, max(H, F)), dtype=torch.int16, device=dev)
+    ops = {}
+    for name, (K, N, res) in shapes.items():
+        nmat = 2 if name == "swiglu" else 1
+        mbytes = nmat * (K * N // 2 + (K // 128) * N * 3)
+        copies = max(2, -(-512 * 2 ** 20 // mbytes))
+        # one seeded matrix per operand, its kernel-native copy written
+        # `copies` times into one allocation (distinct addresses, so the
+        # rotation defeats the Infinity Cache)
+        pk = -(-ss.packed_bytes(K, N) // 256) * 256
+        big = torch.empty(nmat * copies * pk, dtype=torch.uint8, device=dev)
+        canon, descs = [], []
+        for j in range(nmat):
+            q, sc, z = gdev.w4_random_device(9000, j, N, K, device=dev)
+            canon.append((q, sc, z))
+            row = []
+            for c in range(copies):
+                d = ss.make_w4(q, sc, z)
+                view = big[(j * copies + c) * pk:(j * copies + c) * pk + ss.packed_bytes(K, N)]
+                ss.prepack_w4_into(d, view)
+                row.append(d)
+            descs.append(row)
+        xp = torch.zeros(ss.prepared_bytes(M, K), dtype=torch.uint8, device=dev)
+        ws = ss.workspace(max(ss.gemm_workspace_bytes(M, K, N), ss.swiglu_workspace_bytes(M, K, N)), dev)
+        with torch.cuda.stream(stream):
+            ss.prepare_activations(x[:, :K], xp, stream=stream)
+        torch.cuda.synchronize()
+        if name == "swiglu":
+            us = timed(lambda i: ss.w4a16_swiglu_prepared(descs[0][i % copies], descs[1][i % copies], xp, M,
+                                                          y[:, :N], ws, stream=stream))
+        else:
+            r = x[:, :N] if res else None
+            us = timed(lambda i: ss.w4a16_gemm_prepared(descs[0][i % copies], xp, M, y[:, :N], ws, residual=r,
+                                                        stream=stream))
+        ops[name] = {"us": round(us, 2), "bytes": mbytes, "GBps": round(mbytes / (us * 1e-6) / 1e9, 1),
+                     "paper_us": paper[name], "speedup": round(paper[name] / us, 2)}
+        del big, canon, descs
+    # attention: a tree of 8 (spine of 4, branching <= 2), prefix 500 / 1000 / 4096
+    import gen as gen_mod
+    parent = gen_mod.tree(M, 4, 2, 2506)
+    dparent = torch.from_numpy(np.asarray(parent, np.int32)).to(dev)
+    Hd = Hq * D
+    qkv = torch.randint(-3000, 3000, (M, Hd + 2 * Hkv * D), dtype=torch.int16, device=dev) & 0x3BFF
+    out = torch.zeros((M, Hd), dtype=torch.int16, device=dev)
+    for P, paper_us in ((500, 9.6), (1000, 13.4), (4096, 18.8)):
+        S_max = P + M
+        kv_bytes = 2 * Hkv * S_max * D * 2
+        copies = max(2, -(-512 * 2 ** 20 // kv_bytes))
+        kcs = gdev.normal_f16_device(11, P, (copies, Hkv, S_max, D), device=dev)
+        vcs = gdev.normal_f16_device(12, P, (copies, Hkv, S_max, D), device=dev)
+        dP = torch.tensor([P], dtype=torch.int32, device=dev)
+        rope = torch.from_numpy(ss.rope_table(500000.0, S_max, D)).to(dev)
+        ws = ss.workspace(ss.tree_attention_workspace_bytes(M, Hq, Hkv, D, S_max), dev)
+        us = timed(lambda i: ss.tree_attention(qkv, qkv[:, Hd:], qkv[:, Hd + Hkv * D:], kcs[i % copies],
+                                               vcs[i % copies], dP, dparent, Hq, Hkv, D, rope, out, ws,
+                                               stream=stream))
+        ops[f"attention_ctx{P}"] = {"us": round(us, 2), "bytes": kv_bytes, "GBps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
+                                    "paper_us": paper_us, "speedup": round(paper_us / us, 2)}
+        del kcs, vcs
+    torch.cuda.empty_cache()
+    return {"workload": "Llama-3-70B, tensor parallelism 4, batch 8: one GPU's share of each operation "
+                        "(all-reduce not measured)",
+            "paper": "per-operation table (Sec. 2.4; attention there at an unstated context, ~4K implied) and the "
+                     "attention columns of the kernel table (Sec. 5.4, contexts 500 and 1000); H800, BF16",
+            "ops": ops}
 
 
 def draft_side(args, ss, torch, np, dev, stream):

@@ -171,6 +171,14 @@ def prepack_w4(W: W4, stream=None):
     return t
 
 
+def prepack_w4_into(W: W4, out, stream=None):
+    """Fill the caller's uint8 device tensor `out` (at least
+    packed_bytes(K, N) bytes, 16-byte aligned) with the kernel-native copy of
+    W and set W.packed to it."""
+    _check(_load().swiftspec_w4_prepack(ctypes.byref(W), _ptr(out), out.numel(), _stream(stream)), "w4_prepack")
+    W.packed = out.data_ptr()
+
+
 def rope_table(theta: float, S_max: int, D: int):
     """Host fp32 (cos, sin) table [S_max][D/2][2] built in fp64 by the library."""
     import numpy as np

@@ -515,10 +515,12 @@ AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max) {
   const int W = attn_waves(R);
   const int RB = (R + 16 * W - 1) / (16 * W);
   const int groups = Hkv * RB;
-  // about 256 workgroups in flight, at least four key tiles per prefix split
+  // about 256 workgroups in flight, at least two key tiles per prefix split
+  // (four: no change at the 70B shapes, 2 us slower at prefixes of 500-1000
+  // keys with few KV heads; one: slower at 1000 keys)
   int ns = 256 / groups - 1;
   const int max_tiles = (S_max - T + kKeyTile - 1) / kKeyTile;
-  if (ns > max_tiles / 4) ns = max_tiles / 4;
+  if (ns > max_tiles / 2) ns = max_tiles / 2;
   if (ns > kMaxParts - 1) ns = kMaxParts - 1;
   if (ns < 1) ns = 1;
   p.nsplit = ns;

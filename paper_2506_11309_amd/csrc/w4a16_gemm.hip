@@ -40,7 +40,12 @@
 
 namespace ss {
 
-enum { EPI_PLAIN = 0, EPI_SWIGLU = 1 };
+// EPI_SWIGLU_SPLIT: the fused SwiGLU with the gate and the up tile of an
+// output column in two different waves (waves 0, 1: gate tiles of the
+// block's two columns; waves 2, 3: their up tiles), combined through LDS at
+// the end: twice the waves of EPI_SWIGLU for the same columns, half the
+// dequantisation and MFMA work per wave and step.
+enum { EPI_PLAIN = 0, EPI_SWIGLU = 1, EPI_SWIGLU_SPLIT = 2 };
 
 // Kernel-native copy of an int4 matrix (written by prepack_w4_kernel):
 //   q : [N/16 tiles][G groups][64 lanes] x 16 bytes -- lane kq*16 + c holds
@@ -88,6 +93,9 @@ struct GemmShape {
 };
 constexpr GemmShape gemm_shape(int MT, bool swiglu) {
   return MT > 2 ? GemmShape{3, 2, 512} : swiglu ? GemmShape{3, 2, 768} : GemmShape{3, 2, 512};
+}
+constexpr GemmShape gemm_shape_epi(int MT, int EPI) {
+  return EPI == EPI_SWIGLU_SPLIT ? GemmShape{MT == 1 ? 4 : 3, 4, 1 << 30} : gemm_shape(MT, EPI == EPI_SWIGLU);
 }
 constexpr int kRingL = 3;  // LDS ring of activation fragments
 
@@ -168,13 +176,16 @@ __device__ __forceinline__ float* part_slot(const GemmArgs& a, int v, int slot, 
 }
 
 template <int MT, int NWV, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(gemm_shape(MT, EPI == EPI_SWIGLU).occ)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(gemm_shape_epi(MT, EPI).occ)))
 void w4a16_gemm_kernel(GemmArgs a) {
+  constexpr bool kSplit = EPI == EPI_SWIGLU_SPLIT;
   constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;  // output column tiles per wave
-  constexpr int kColB = 4 * kColW;                             // output column tiles per block
+  constexpr int kColB = kSplit ? 2 : 4 * kColW;                // output column tiles per block
   constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;
-  constexpr int kRing = gemm_shape(MT, EPI == EPI_SWIGLU).ring;
+  constexpr int kRing = gemm_shape_epi(MT, EPI).ring;
+  static_assert(!kSplit || NWV == 1, "split SwiGLU: one tile per wave");
   __shared__ u32x4 abuf[kRingL][MT][4][kWave];  // activation fragments of 3 groups
+  __shared__ f32x4 xch[kSplit ? 2 : 1][MT][kWave];  // split SwiGLU: the up sums for the gate waves
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -206,15 +217,15 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // so a load costs no vector ALU work.
   const uint32_t q_bytes = (uint32_t)((size_t)a.K * a.N / 2), sz_bytes = (uint32_t)((size_t)a.N * G * 4);
   const auto rq0 = buffer_rsrc(a.w0.q, q_bytes), rs0 = buffer_rsrc(a.w0.sz, sz_bytes);
-  const auto rq1 = buffer_rsrc(EPI == EPI_SWIGLU ? a.w1.q : a.w0.q, q_bytes);
-  const auto rs1 = buffer_rsrc(EPI == EPI_SWIGLU ? a.w1.sz : a.w0.sz, sz_bytes);
+  const auto rq1 = buffer_rsrc(EPI != EPI_PLAIN ? a.w1.q : a.w0.q, q_bytes);
+  const auto rs1 = buffer_rsrc(EPI != EPI_PLAIN ? a.w1.sz : a.w0.sz, sz_bytes);
   const auto ra = buffer_rsrc(a.a, (uint32_t)(MT * G * 4 * kWave * 16));
   const uint32_t lane16 = (uint32_t)lane * 16u, col4 = (uint32_t)ncol * 4u;
   auto load_b = [&](BStage<MT, NWV>& st) {
-    const int tw = ld_nb * kColB + wave * kColW;  // first column tile of this wave
+    const int tw = ld_nb * kColB + (kSplit ? (wave & 1) : wave * kColW);  // first column tile of this wave
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
-      const bool up = EPI == EPI_SWIGLU && nt >= kColW;
+      const bool up = (EPI == EPI_SWIGLU && nt >= kColW) || (kSplit && wave >= 2);
       const uint32_t tg = (uint32_t)((tw + nt % kColW) * G + ld_g);
       st.b[nt] = buffer_load_x4(up ? rq1 : rq0, lane16, tg * 1024u);
       st.sz[nt] = buffer_load_x1(up ? rs1 : rs0, col4, tg * 64u);
@@ -308,10 +319,6 @@ void w4a16_gemm_kernel(GemmArgs a) {
   };
   // End of an N-block's share inside the range: write the outputs if the
   // range holds the whole N-block, else publish the partial (slot 0: the
-  // range's first N-block, slot 1: its last) without waiting; tickets are
-  // taken once at the end of the range.
-  // End of an N-block's share inside the range: write the outputs if the
-  // range holds the whole N-block, else publish the partial (slot 0: the
   // range's first N-block, slot 1: its last) for the fix-up kernel.
   auto flush = [&](int nb) {
 #pragma unroll
@@ -319,7 +326,35 @@ void w4a16_gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] *= 0.0625f;  // the 16 of C_g, exactly
     const bool full = (long)nb * G >= u_lo && (long)(nb + 1) * G <= u_hi;
-    if (full) {
+    if constexpr (kSplit) {
+      // every range holds whole blocks: the up waves hand their sums to the
+      // gate waves of the same columns, which write silu(gate) * up
+      if (wave >= 2) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) xch[wave - 2][mt][lane] = acc[mt][0];
+      }
+      __syncthreads();
+      if (wave < 2) {
+        const int col = (nb * kColB + wave) * 16 + ncol;
+        const int G2 = a.N >> 7;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const f32x4 u = xch[wave][mt][lane];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = mt * 16 + kq * 4 + r;
+            if (m < a.M) {
+              const float gte = acc[mt][0][r];
+              const uint16_t h = f2h(gte / (1.0f + __expf(-gte)) * u[r]);
+              if (a.y) a.y[(size_t)m * a.ldy + col] = h;
+              if (a.yp) store_prepared(a.yp, m, col, G2, h);
+            }
+          }
+        }
+      }
+      __syncthreads();  // the exchange buffer is free for the range's next block
+      (void)full;
+    } else if (full) {
       emit(nb);
     } else {
       float* mine = part_slot<MT, NWV, EPI>(a, v, nb == u_lo / G ? 0 : 1, wave);
@@ -370,7 +405,7 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // barrier of step i has passed) and applies unit i - 1's sums.  Above 32
   // rows the second buffers would cost the second wave per SIMD, so step i
   // reads, multiplies and applies its own unit.
-  constexpr bool kPipe = MT <= 2;
+  constexpr bool kPipe = MT <= 2 && !kSplit;
   constexpr int kBuf = kPipe ? 2 : 1;
   half8 af[kBuf][MT][4];
   f32x4 cs[kBuf][MT][NWV];
@@ -575,16 +610,26 @@ static void launch_t(const GemmLaunch& L, hipStream_t st) {
   a.units = (long)L.nblocks * a.G;
   a.part = L.part;
   hipLaunchKernelGGL((w4a16_gemm_kernel<MT, NW, EPI>), dim3(L.nwg), dim3(256), 0, st, a);
-  // ranges split no N-block when every workgroup gets whole N-blocks
-  if (L.nblocks % L.nwg != 0)
-    hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks), dim3(256), 0, st, a);
+  // ranges split no N-block when every workgroup gets whole N-blocks (the
+  // split SwiGLU is only planned that way)
+  if constexpr (EPI != EPI_SWIGLU_SPLIT) {
+    if (L.nblocks % L.nwg != 0)
+      hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks), dim3(256), 0, st, a);
+  }
 }
 
-// instantiated shapes: SwiGLU one gate + one up tile per wave; plain one or
+// instantiated shapes: SwiGLU one gate + one up tile per wave, or (up to 32
+// rows) one tile per wave with gate and up in different waves; plain one or
 // two tiles per wave
 template <int MT, int EPI>
 static void launch_nw(const GemmLaunch& L, hipStream_t st) {
   if constexpr (EPI == EPI_SWIGLU) {
+    if constexpr (MT <= 2) {
+      if (L.nw == 1) {
+        launch_t<MT, 1, EPI_SWIGLU_SPLIT>(L, st);
+        return;
+      }
+    }
     launch_t<MT, 2, EPI>(L, st);
   } else if constexpr (MT <= 2) {
     if (L.nw == 2) launch_t<MT, 2, EPI>(L, st);
@@ -616,6 +661,20 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
   GemmPlan p;
   const int tiles = N / 16;
   const int MT = (M + 15) / 16;
+  if (swiglu && MT <= 2 && tiles % 2 == 0 && tiles / 4 < 256 && tiles / 2 >= 256) {
+    // gate and up tiles in different waves, one workgroup per 2 columns:
+    // where the 4-column blocks are too few to fill the chip on their own
+    // (the 8B width: 224 blocks, 20.5 -> 18 us at 16 rows; the 1B width:
+    // 128 blocks, 14.3 -> 9.2 us at 8 rows) this replaces stream-K and its
+    // fix-up; at the 70B width (448 blocks) it is slower, 56 -> 72 us at 32
+    // rows, as every workgroup reads the activations for half the columns
+    p.nw = 1;
+    p.nblocks = tiles / 2;
+    p.nwg = p.nblocks;
+    p.part_bytes = 0;
+    p.prep_bytes = (size_t)MT * (K / 128) * 4 * kWave * 16;
+    return p;
+  }
   if (swiglu) {
     p.nw = 2;  // one gate and one up tile per wave
     p.nblocks = tiles / 4;

@@ -264,6 +264,31 @@ def test_w4a16_swiglu_70b_width(M):
     check_close(y[:, cols], ref, f"swiglu 70b width M={M}")
 
 
+@pytest.mark.parametrize("M,K,N", [(16, 4096, 14336), (1, 4096, 14336), (17, 4096, 14336), (32, 4096, 14336),
+                                   (8, 2048, 8192), (31, 2048, 8192)])
+def test_w4a16_swiglu_two_column_blocks(M, K, N):
+    """SwiGLU at the 8B and 1B FFN widths, where the gate and up tiles of a
+    column run in different waves of one workgroup: sampled columns (the first
+    and last 64, 256 random ones) against the oracle, and two calls agree bit
+    for bit."""
+    Wg, Wu = _rand_w4(31 + M, N, K), _rand_w4(32 + M, N, K)
+    x = gen.normal_f16(33, M, (M, K))
+    tg, dg = upload_w4(Wg)
+    tu, du = upload_w4(Wu)
+    outs = []
+    for _ in range(2):
+        dy = torch.zeros((M, N), dtype=torch.int16, device=dev())
+        ws = ss.workspace(ss.swiglu_workspace_bytes(M, K, N), dev())
+        ss.w4a16_swiglu(dg, du, up(x), dy, ws)
+        torch.cuda.synchronize()
+        outs.append(down16(dy))
+    assert np.array_equal(outs[0], outs[1])
+    cols = np.concatenate([np.arange(64), np.arange(N - 64, N),
+                           np.random.default_rng(34).choice(np.arange(64, N - 64), 256, replace=False)])
+    ref = oracle.w4a16_swiglu(_w4_rows(Wg, cols), _w4_rows(Wu, cols), x)
+    check_close(outs[0][:, cols], ref, f"swiglu M={M} K={K} N={N}")
+
+
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 1024), (8, 2048, 512), (13, 1024, 2048), (32, 8192, 1024),
                                    (40, 4096, 1024), (64, 2048, 1024)])
 def test_w4a16_gemm_valu_variant_matches_oracle(M, K, N):

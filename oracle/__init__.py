@@ -71,6 +71,8 @@ def _load():
     lib.oracle_kv_reorganize.restype = i32
     lib.oracle_greedy_accept.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.oracle_greedy_accept.restype = i32
+    lib.oracle_topk_logprobs.argtypes = [vp, i32, i32, i32, i32, vp, vp]
+    lib.oracle_topk_logprobs.restype = i32
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -294,6 +296,18 @@ def greedy_accept(logits, tokens, parent):
     if L < 0:
         raise ValueError("oracle_greedy_accept: invalid arguments or tree")
     return am, int(acc[0]), int(bon[0]), int(L)
+
+
+def topk_logprobs(logits, k):
+    """The k most probable next tokens of each logits row (ties: lower index
+    first) and their log-softmax values: (tokens [n][k] int32, logprobs
+    [n][k] float64)."""
+    lg = _c(logits, np.uint16)
+    n, V = lg.shape
+    tok = np.zeros((n, k), np.int32)
+    lp = np.zeros((n, k), np.float64)
+    assert _load().oracle_topk_logprobs(_p(lg), n, V, V, k, _p(tok), _p(lp)) == 0
+    return tok, lp
 
 
 def num_threads() -> int:

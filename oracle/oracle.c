@@ -491,6 +491,44 @@ int32_t oracle_greedy_accept(const uint16_t* logits, int32_t T, int32_t V, int32
   return L;
 }
 
+/* ------------------------------------------- draft expansion: top-k children */
+
+int32_t oracle_topk_logprobs(const uint16_t* logits, int32_t n, int32_t V, int32_t ldl, int32_t k,
+                             int32_t* tokens, double* logprobs) {
+  if (n < 0 || V < 1 || ldl < V || k < 1 || k > V) return -1;
+  for (int32_t i = 0; i < n; ++i) {
+    const uint16_t* row = logits + (size_t)i * ldl;
+    /* log-softmax: x - max - log(sum exp(x - max)) */
+    double mx = oracle_f16_to_f64(row[0]);
+    for (int32_t v = 1; v < V; ++v) {
+      const double x = oracle_f16_to_f64(row[v]);
+      if (x > mx) mx = x;
+    }
+    double se = 0.0;
+    for (int32_t v = 0; v < V; ++v) se += exp(oracle_f16_to_f64(row[v]) - mx);
+    const double lse = mx + log(se);
+    /* the k most probable tokens, one at a time: the largest logit not yet
+     * taken, the lower index first among equal logits */
+    for (int32_t j = 0; j < k; ++j) {
+      int32_t best = -1;
+      double bv = 0.0;
+      for (int32_t v = 0; v < V; ++v) {
+        int taken = 0;
+        for (int32_t q = 0; q < j; ++q) taken |= tokens[(size_t)i * k + q] == v;
+        if (taken) continue;
+        const double x = oracle_f16_to_f64(row[v]);
+        if (best < 0 || x > bv) {
+          best = v;
+          bv = x;
+        }
+      }
+      tokens[(size_t)i * k + j] = best;
+      logprobs[(size_t)i * k + j] = bv - lse;
+    }
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------------- layer */
 
 int oracle_verify_layer(const oracle_dims* dims, const uint16_t* attn_norm,

@@ -160,6 +160,13 @@ int oracle_verify_layer(const oracle_dims* dims, const uint16_t* attn_norm,
 int oracle_lm_head(const uint16_t* h, int32_t M, int32_t H, const uint16_t* gamma, double eps,
                    const uint16_t* W, int32_t V, uint16_t* logits);
 
+/* Draft-tree expansion (Sec. 3.1, maximum-likelihood expansion): for each
+ * of n logits rows [V] fp16 (stride ldl), the k tokens of largest logit
+ * (equal logits: lower index first) and their log-softmax values.  O(k V)
+ * per row.  Returns 0 or -1. */
+int32_t oracle_topk_logprobs(const uint16_t* logits, int32_t n, int32_t V, int32_t ldl, int32_t k,
+                             int32_t* tokens, double* logprobs);
+
 int oracle_num_threads(void);
 
 #ifdef __cplusplus

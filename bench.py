@@ -476,9 +476,18 @@ def draft_side(args, ss, torch, np, dev, stream):
                                                     stream=stream))
     reorg_us = timed(lambda: ss.kv_reorganize(kc, vc, dP, dcp, last, keep, new_parent=newp, n_kept=nk,
                                               n_layers=n_layers, advance=False, ws=ws, stream=stream))
+    # expansion: the k = 8 most probable children of each of the w leaves
+    # (top-k log-softmax over the draft's 128256-entry vocabulary)
+    V, k = 128256, 8
+    dlg = gdev.normal_f16_device(7, 5, (w, V), device=dev)
+    dtok = torch.zeros((w, k), dtype=torch.int32, device=dev)
+    dlp = torch.zeros((w, k), dtype=torch.float32, device=dev)
+    ws_k = ss.workspace(ss.topk_logprobs_workspace_bytes(w), dev)
+    topk_us = timed(lambda: ss.topk_logprobs(dlg, dtok, dlp, ws_k, stream=stream))
     if ss.read_device_error(ws, stream):
         raise RuntimeError("device error in the draft-side kernels")
     kept = int(nk.item())
+    host = draft_tree_host(ss, np, w=w, k=k)
     attn_bytes = 2 * s.Hkv * (P + N + w) * s.D * 2   # K and V rows read (upper bound: every tree row)
     reorg_bytes = n_layers * 2 * s.Hkv * (3 + kept) * s.D * 2 * 2
     return {"workload": f"Llama-3.2-1B-shaped draft ({n_layers} layers, Hq/Hkv={s.Hq}/{s.Hkv}, D={s.D}); "
@@ -486,7 +495,66 @@ def draft_side(args, ss, torch, np, dev, stream):
             "draft_attention_us": round(attn_us, 2),
             "draft_attention_gbs": round(attn_bytes / (attn_us * 1e-6) / 1e9, 1),
             "kv_reorganize_all_layers_us": round(reorg_us, 2),
-            "kv_reorganize_bytes": reorg_bytes}
+            "kv_reorganize_bytes": reorg_bytes,
+            "topk_logprobs_us": round(topk_us, 2),
+            "topk_logprobs_gbs": round(w * V * 2 / (topk_us * 1e-6) / 1e9, 1),
+            "draft_tree_host": host}
+
+
+def draft_tree_host(ss, np, w=8, k=8, d=3, bs=8, iters=200, vocab=128256):
+    """The draft worker's host-side tree (swiftspec_draft_tree_*, through the
+    Python binding) over `iters` iterations of the loop of Alg. 1: d
+    expansion steps of w leaves with k children each (synthetic
+    log-probabilities, seeded), re-rooting on a synthetic target output (the
+    root path to a node drawn at random plus one token, a child's 70 % of
+    the time), growth to bs nodes, and the bs-node subgraph; tree-cache rows
+    capped at 64 (the draft kernels' limit).  Mean microseconds per call."""
+    import time
+    rng = np.random.default_rng(11309)
+    tree = ss.DraftTree(1 << 16, 1)
+    t_exp = t_rr = t_sub = 0.0
+    n_exp = 0
+    sizes = []
+    lps = [(-np.sort(-np.log(rng.dirichlet(np.full(64, 0.3))))[:k]).astype(np.float32) for _ in range(64)]
+    toks = rng.integers(0, vocab, (4096, k)).astype(np.int32)
+    for it in range(iters):
+        for _ in range(d):
+            if tree.rows() + w > 64:
+                break
+            t0 = time.perf_counter()
+            leaves, _ = tree.select_leaves(w)
+            n = len(leaves)
+            tree.expand(leaves, toks[(it * 7 + n_exp) % 4000:(it * 7 + n_exp) % 4000 + n],
+                        np.stack([lps[(it + j) % 64] for j in range(n)]))
+            t_exp += time.perf_counter() - t0
+            n_exp += 1
+        sizes.append(tree.size())
+        tok_h, par_h, _, _, _ = tree.nodes()
+        v = int(rng.integers(len(tok_h)))
+        path = []
+        while v >= 0:
+            path.append(v)
+            v = int(par_h[v])
+        ver = [int(tok_h[u]) for u in path[::-1]]
+        kids = np.nonzero(par_h == path[0])[0]
+        ver.append(int(tok_h[kids[0]]) if len(kids) and rng.random() < 0.7 else vocab + 1)
+        t0 = time.perf_counter()
+        tree.reroot(ver)
+        t_rr += time.perf_counter() - t0
+        while tree.size() < bs and tree.rows() + w <= 64:
+            t0 = time.perf_counter()
+            leaves, _ = tree.select_leaves(w)
+            tree.expand(leaves, toks[:len(leaves)], np.stack([lps[j] for j in range(len(leaves))]))
+            t_exp += time.perf_counter() - t0
+            n_exp += 1
+        t0 = time.perf_counter()
+        tree.select_subgraph(bs)
+        t_sub += time.perf_counter() - t0
+    return {"iterations": iters, "w": w, "k": k, "d": d, "bs": bs,
+            "mean_tree_nodes": round(float(np.mean(sizes)), 1),
+            "expand_step_us": round(t_exp / max(n_exp, 1) * 1e6, 2),
+            "reroot_us": round(t_rr / iters * 1e6, 2),
+            "select_subgraph_us": round(t_sub / iters * 1e6, 2)}
 
 
 def full_step(args, ss, torch, np, dev, stream):

@@ -65,7 +65,8 @@ enum {
   SWIFTSPEC_MISALIGNED = 3,          /* pointer or leading dimension breaks 16-byte alignment */
   SWIFTSPEC_WORKSPACE_TOO_SMALL = 4, /* ws_bytes below the *_workspace_bytes figure */
   SWIFTSPEC_BAD_TREE = 5,            /* host-side tree validation failed */
-  SWIFTSPEC_HIP_ERROR = 6            /* a HIP runtime call failed; see swiftspec_last_hip_error */
+  SWIFTSPEC_HIP_ERROR = 6,           /* a HIP runtime call failed; see swiftspec_last_hip_error */
+  SWIFTSPEC_CAPACITY = 7             /* a host-side draft tree would exceed its node capacity */
 };
 
 /* bits of the device error word */
@@ -269,6 +270,97 @@ int swiftspec_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_laye
                             int32_t Hkv, int32_t S_max, int32_t D, int32_t* d_prefix_len, const int32_t* d_parent,
                             int32_t N, const int32_t* d_last, const int32_t* d_keep, int32_t* d_new_parent,
                             int32_t* d_n_kept, int32_t advance, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------ draft tree expansion
+ * The children of the leaves a draft step expands (Sec. 3.1, maximum-
+ * likelihood tree expansion: a node's value is the log-softmax probability
+ * of its token): for each of n logits rows [V] fp16 (row i at
+ * logits + i * ldl, device), the k tokens of largest logit (equal logits:
+ * lower index first) into d_tokens[n][k] (int32, device) and their
+ * log-softmax values, computed in fp32, into d_logprobs[n][k] (float,
+ * device), in decreasing order.  Logits are expected to be finite.
+ * 1 <= n <= 64, 1 <= k <= 8, k <= V, ldl >= V, ldl % 8 == 0, logits 16-byte
+ * aligned.  ws: swiftspec_topk_logprobs_workspace_bytes(n) bytes (per-range
+ * partial lists after the header; the header's counters are used and left
+ * zero). */
+size_t swiftspec_topk_logprobs_workspace_bytes(int32_t n);
+int swiftspec_topk_logprobs(const uint16_t* logits, int32_t ldl, int32_t n, int32_t V, int32_t k,
+                            int32_t* d_tokens, float* d_logprobs, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------- draft tree (host)
+ * The draft worker's tree of parallel tree generation (Sec. 3.1, Alg. 1;
+ * re-rooting and the draft cache per Sec. 3.2 and Fig. 5).  HOST memory
+ * and host computation only; no call touches the GPU.  Not thread-safe.
+ *
+ * Node 0 is the root; children get the next indices (parents precede
+ * children).  A node's value is a log-probability (<= 0) and its weight the
+ * sum of values from the root (double; the root's weight is 0).  The order
+ * used everywhere: larger weight first, then lower index.
+ * Draft cache: the root's keys and values are the last row of the draft's
+ * prefix cache (once the root is expanded); every other node selected for
+ * expansion owns one tree-cache row (rows 0, 1, ... in selection order; the
+ * draft attention of those leaves writes them, swiftspec_draft_tree_attention
+ * with the forest below as d_cache_parent).
+ *
+ * create: an empty tree of capacity nodes holding the root token (not yet
+ *   expanded).  destroy: frees it.  size / rows: nodes / tree-cache rows
+ *   (-1 for NULL).
+ * nodes: copies token, parent, weight, row (-1: none) and expanded (0/1)
+ *   of every node into the non-NULL host arrays of size() entries.
+ * forest: parent_row[rows()] = the tree-cache row of each row's parent, -1
+ *   for a child of the root.
+ * select_leaves: the up to w unexpanded, unselected nodes first in the
+ *   order (a priority queue, O(w log s)) into leaves[*n]; each non-root one
+ *   gets the next tree-cache row; parent_row[j] = its parent's row (-1: the
+ *   root).  They stay selected until expanded.
+ * expand: for j < n, leaf leaves[j] (selected, not yet expanded) receives
+ *   children tokens[j][0..k) with values logprobs[j][0..k) (each <= 0,
+ *   e.g. the output of swiftspec_topk_logprobs copied to the host), appended
+ *   in leaf order then child order.  Everything is checked first:
+ *   SWIFTSPEC_INVALID_ARG (bad leaf, repeated leaf, value > 0 or NaN) or
+ *   SWIFTSPEC_CAPACITY leaves the tree unchanged.
+ * select_subgraph: the min(bs, size) nodes first in the order -- the most
+ *   probable connected subgraph containing the root -- listed by node index
+ *   into nodes[*n], with parent[j] = the position of node j's parent in that
+ *   list (-1 for the root) and tokens[j] (nullable): a tree for
+ *   swiftspec_verify_step.
+ * reroot: verified[0 .. n_verified) = the target's output (root token
+ *   first, then the accepted tokens and the token the target produced after
+ *   them, as in the walk-through of Fig. 3; n_verified >= 2).  From the root the walk goes
+ *   to the (lowest-index) child carrying the next verified token while there
+ *   is one; *last = the tree-cache row of the deepest walked node owning one
+ *   (-1: none) and *path_rows = the walked nodes owning rows (they move to
+ *   the prefix).  If the walk consumed every verified token and ended on an
+ *   expanded non-root node, that node becomes the root and its subtree is
+ *   kept (nodes renumbered in index order, rows in row order, weights minus
+ *   its weight): *keep = 1, *n_pending = 0.  Otherwise the tree restarts
+ *   from a fresh root holding the last verified token: *keep = 0 and
+ *   pending[*n_pending] (at most n_verified entries) = the tokens whose
+ *   draft keys and values are still missing, in context order: the old root
+ *   if it was never expanded, then the verified tokens after the walked
+ *   nodes owning rows (the last is the new root).  *last, *keep and the
+ *   forest before the call are the arguments of swiftspec_kv_reorganize for
+ *   the draft cache.  SWIFTSPEC_INVALID_ARG if n_verified < 2, if
+ *   verified[0] is not the root
+ *   token, if a verified token other than the last is not found, or if
+ *   selected leaves are still unexpanded; the tree is then unchanged. */
+typedef struct swiftspec_draft_tree swiftspec_draft_tree;
+int swiftspec_draft_tree_create(int32_t capacity, int32_t root_token, swiftspec_draft_tree** out);
+void swiftspec_draft_tree_destroy(swiftspec_draft_tree* t);
+int32_t swiftspec_draft_tree_size(const swiftspec_draft_tree* t);
+int32_t swiftspec_draft_tree_rows(const swiftspec_draft_tree* t);
+int swiftspec_draft_tree_nodes(const swiftspec_draft_tree* t, int32_t* token, int32_t* parent, double* weight,
+                               int32_t* row, int32_t* expanded);
+int swiftspec_draft_tree_forest(const swiftspec_draft_tree* t, int32_t* parent_row);
+int swiftspec_draft_tree_select_leaves(swiftspec_draft_tree* t, int32_t w, int32_t* leaves, int32_t* parent_row,
+                                       int32_t* n);
+int swiftspec_draft_tree_expand(swiftspec_draft_tree* t, int32_t n, const int32_t* leaves, int32_t k,
+                                const int32_t* tokens, const float* logprobs);
+int swiftspec_draft_tree_select_subgraph(const swiftspec_draft_tree* t, int32_t bs, int32_t* nodes,
+                                         int32_t* parent, int32_t* tokens, int32_t* n);
+int swiftspec_draft_tree_reroot(swiftspec_draft_tree* t, const int32_t* verified, int32_t n_verified,
+                                int32_t* last, int32_t* path_rows, int32_t* keep, int32_t* pending,
+                                int32_t* n_pending);
 
 /* ------------------------------------------------- greedy acceptance
  * Closes a verification step on the device (Sec. 3.1, Fig. 3 walk-through:

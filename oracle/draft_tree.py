@@ -125,7 +125,8 @@ class DraftTree:
         subtree below `last` is kept), pending (tokens whose draft keys and
         values are still to be computed, in context order)."""
         verified = [int(t) for t in verified]
-        assert len(verified) >= 1 and verified[0] == self.token[0]
+        # an output holds the root and at least the token after it
+        assert len(verified) >= 2 and verified[0] == self.token[0]
         assert not any(self.selected)
         walked = [0]
         for t in verified[1:]:

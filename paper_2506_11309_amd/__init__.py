@@ -24,7 +24,7 @@ _lib = None
 i32, i64, f32, f64, vp, sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
                               ctypes.c_void_p, ctypes.c_size_t)
 
-OK, INVALID_ARG, UNSUPPORTED, MISALIGNED, WORKSPACE_TOO_SMALL, BAD_TREE, HIP_ERROR = range(7)
+OK, INVALID_ARG, UNSUPPORTED, MISALIGNED, WORKSPACE_TOO_SMALL, BAD_TREE, HIP_ERROR, CAPACITY = range(8)
 DEVERR_BAD_TREE, DEVERR_BAD_PREFIX, DEVERR_BAD_ACCEPTED = 1, 2, 4
 WS_HEADER_BYTES = 65536
 MAX_TREE = 64
@@ -62,6 +62,18 @@ _SIGS = {
                                         f32, vp, i32, vp, sz, vp], ctypes.c_int),
     "swiftspec_kv_reorganize": ([vp, vp, i32, i64, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp, i32, vp, sz, vp],
                                 ctypes.c_int),
+    "swiftspec_topk_logprobs_workspace_bytes": ([i32], sz),
+    "swiftspec_topk_logprobs": ([vp, i32, i32, i32, i32, vp, vp, vp, sz, vp], ctypes.c_int),
+    "swiftspec_draft_tree_create": ([i32, i32, ctypes.POINTER(vp)], ctypes.c_int),
+    "swiftspec_draft_tree_destroy": ([vp], None),
+    "swiftspec_draft_tree_size": ([vp], i32),
+    "swiftspec_draft_tree_rows": ([vp], i32),
+    "swiftspec_draft_tree_nodes": ([vp, vp, vp, vp, vp, vp], ctypes.c_int),
+    "swiftspec_draft_tree_forest": ([vp, vp], ctypes.c_int),
+    "swiftspec_draft_tree_select_leaves": ([vp, i32, vp, vp, vp], ctypes.c_int),
+    "swiftspec_draft_tree_expand": ([vp, i32, vp, i32, vp, vp], ctypes.c_int),
+    "swiftspec_draft_tree_select_subgraph": ([vp, i32, vp, vp, vp, vp], ctypes.c_int),
+    "swiftspec_draft_tree_reroot": ([vp, vp, i32, vp, vp, vp, vp, vp], ctypes.c_int),
     "swiftspec_greedy_accept_workspace_bytes": ([i32], sz),
     "swiftspec_greedy_accept": ([vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     "swiftspec_read_device_error": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
@@ -362,6 +374,103 @@ def greedy_accept(logits, tokens, parent, argmax, accepted, bonus, ws, path_len=
                                          _ptr(path_len), _ptr(ws), ws.numel() if ws is not None else 0,
                                          _stream(stream))
     _check(st, "greedy_accept")
+
+
+def topk_logprobs_workspace_bytes(n) -> int:
+    return int(_load().swiftspec_topk_logprobs_workspace_bytes(n))
+
+
+def topk_logprobs(logits, tokens, logprobs, ws, V=None, stream=None):
+    """logits [n][ldl] fp16 (first V columns; default all) -> the k most
+    probable tokens of each row (device int32 tokens [n][k]) and their
+    log-softmax values (device float32 logprobs [n][k])."""
+    n, ldl = logits.shape
+    k = tokens.shape[1]
+    st = _load().swiftspec_topk_logprobs(_ptr(logits), ldl, n, ldl if V is None else V, k, _ptr(tokens),
+                                         _ptr(logprobs), _ptr(ws), ws.numel() if ws is not None else 0,
+                                         _stream(stream))
+    _check(st, "topk_logprobs")
+
+
+class DraftTree:
+    """Host-side draft tree (swiftspec_draft_tree_*): host numpy arrays in
+    and out, no device work."""
+
+    def __init__(self, capacity: int, root_token: int):
+        import numpy as np
+        self._np = np
+        h = vp()
+        _check(_load().swiftspec_draft_tree_create(capacity, root_token, ctypes.byref(h)), "draft_tree_create")
+        self._h = h
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.swiftspec_draft_tree_destroy(self._h)
+            self._h = None
+
+    def _a(self, n, dtype):
+        return self._np.zeros(max(int(n), 1), dtype)
+
+    @staticmethod
+    def _p(a):
+        return a.ctypes.data if a is not None else None
+
+    def size(self) -> int:
+        return int(_load().swiftspec_draft_tree_size(self._h))
+
+    def rows(self) -> int:
+        return int(_load().swiftspec_draft_tree_rows(self._h))
+
+    def nodes(self):
+        """(token, parent, weight, row, expanded) arrays over all nodes."""
+        np = self._np
+        n = self.size()
+        tok, par, row, exp = (self._a(n, np.int32) for _ in range(4))
+        w = self._a(n, np.float64)
+        _check(_load().swiftspec_draft_tree_nodes(self._h, self._p(tok), self._p(par), self._p(w), self._p(row),
+                                                  self._p(exp)), "draft_tree_nodes")
+        return tok[:n], par[:n], w[:n], row[:n], exp[:n]
+
+    def forest(self):
+        f = self._a(self.rows(), self._np.int32)
+        _check(_load().swiftspec_draft_tree_forest(self._h, self._p(f)), "draft_tree_forest")
+        return f[:self.rows()]
+
+    def select_leaves(self, w: int):
+        np = self._np
+        leaves, prow, n = self._a(w, np.int32), self._a(w, np.int32), np.zeros(1, np.int32)
+        _check(_load().swiftspec_draft_tree_select_leaves(self._h, w, self._p(leaves), self._p(prow),
+                                                          self._p(n)), "draft_tree_select_leaves")
+        return leaves[:n[0]], prow[:n[0]]
+
+    def expand(self, leaves, tokens, logprobs):
+        np = self._np
+        leaves = np.ascontiguousarray(leaves, np.int32)
+        tokens = np.ascontiguousarray(tokens, np.int32).reshape(len(leaves), -1)
+        logprobs = np.ascontiguousarray(logprobs, np.float32).reshape(len(leaves), -1)
+        _check(_load().swiftspec_draft_tree_expand(self._h, len(leaves), self._p(leaves), tokens.shape[1],
+                                                   self._p(tokens), self._p(logprobs)), "draft_tree_expand")
+
+    def select_subgraph(self, bs: int):
+        """(nodes, parent positions, tokens) of the bs most probable nodes."""
+        np = self._np
+        nodes, par, tok, n = self._a(bs, np.int32), self._a(bs, np.int32), self._a(bs, np.int32), np.zeros(1, np.int32)
+        _check(_load().swiftspec_draft_tree_select_subgraph(self._h, bs, self._p(nodes), self._p(par), self._p(tok),
+                                                            self._p(n)), "draft_tree_select_subgraph")
+        m = int(n[0])
+        return nodes[:m], par[:m], tok[:m]
+
+    def reroot(self, verified):
+        """dict(last, path_rows, keep, pending) as swiftspec_draft_tree_reroot."""
+        np = self._np
+        ver = np.ascontiguousarray(verified, np.int32)
+        out = np.zeros(4, np.int32)
+        pend = self._a(len(ver), np.int32)
+        _check(_load().swiftspec_draft_tree_reroot(self._h, self._p(ver), len(ver), self._p(out[0:1]),
+                                                   self._p(out[1:2]), self._p(out[2:3]), self._p(pend),
+                                                   self._p(out[3:4])), "draft_tree_reroot")
+        return {"last": int(out[0]), "path_rows": int(out[1]), "keep": int(out[2]),
+                "pending": [int(x) for x in pend[:out[3]]]}
 
 
 def make_dims(H, Hq, Hkv, D, F, S_max, eps=1e-5, rope_theta=500000.0) -> Dims:

@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(BUILD, "libswiftspec.so")
-SOURCES = ["w4a16_gemm.hip", "tree_attention.hip", "small_kernels.hip", "lm_head.hip", "w4a16_gemm_valu.hip", "greedy_accept.hip", "swiftspec_api.cpp"]
+SOURCES = ["w4a16_gemm.hip", "tree_attention.hip", "small_kernels.hip", "lm_head.hip", "w4a16_gemm_valu.hip", "greedy_accept.hip", "draft_expand.hip", "draft_tree.cpp",
+           "swiftspec_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

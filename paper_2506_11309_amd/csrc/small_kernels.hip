@@ -6,28 +6,49 @@ namespace ss {
 
 // ------------------------------------------------------------------ RMSNorm
 // out = fp16(x / sqrt(mean(x^2) + eps) * gamma); one workgroup per row,
-// fp32 sum of squares, fixed reduction order (deterministic).
+// fp32 sum of squares, fixed reduction order (deterministic).  Thread t owns
+// the 32-element chunks c = t + 256 i (k = 32 c .. 32 c + 31), i.e. one
+// prepared fragment set each.  With kRegs > 0 (rows of at most 8192 kRegs
+// elements) the row and gamma are loaded once, up front, and kept in
+// registers across the reduction; kRegs = 0 re-reads them (any width).
+template <int kRegs>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x, int H, int ldx,
                                                       const uint16_t* __restrict__ gamma, float eps,
                                                       uint16_t* __restrict__ out, int ldo,
                                                       uint16_t* __restrict__ out_prep) {
-  // one workgroup per row; thread t owns the 32-element chunks c = t + 256 i
-  // (k = 32 c .. 32 c + 31), i.e. one prepared fragment set each
   __shared__ float partial[4];
   const int m = blockIdx.x;
   const uint16_t* xr = x + (size_t)m * ldx;
   const int nch = H >> 5;
+  constexpr int kR = kRegs > 0 ? kRegs : 1;
+  u32x4 xv[kR][4], gv[kR][4];
+  auto sumsq = [](const u32x4& v, float& acc) {
+    const half8 h = bitcast<half8>(v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)h[e], (float)h[e], acc);
+  };
   float ss = 0.f;
-  for (int c = threadIdx.x; c < nch; c += 256) {
+  if constexpr (kRegs > 0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q));
+    for (int i = 0; i < kRegs; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      if (c < nch) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float v = (float)h[e];
-        ss = __builtin_fmaf(v, v, ss);
+        for (int q = 0; q < 4; ++q) {
+          xv[i][q] = *reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q);
+          gv[i][q] = *reinterpret_cast<const u32x4*>(gamma + 32 * c + 8 * q);
+        }
       }
     }
+#pragma unroll
+    for (int i = 0; i < kRegs; ++i)
+      if (threadIdx.x + 256 * i < nch)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) sumsq(xv[i][q], ss);
+  } else {
+    for (int c = threadIdx.x; c < nch; c += 256)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sumsq(*reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q), ss);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, kWave);
@@ -37,12 +58,12 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
   const float inv = 1.0f / sqrtf(total / (float)H + eps);
   uint16_t* orow = out + (size_t)m * ldo;
   const int G = H >> 7;
-  for (int c = threadIdx.x; c < nch; c += 256) {
+  auto emit = [&](int c, const u32x4 (&xs)[4], const u32x4 (&gs)[4]) {
     uint32_t w[16];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const half8 h = bitcast<half8>(*reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q));
-      const half8 gm = bitcast<half8>(*reinterpret_cast<const u32x4*>(gamma + 32 * c + 8 * q));
+      const half8 h = bitcast<half8>(xs[q]);
+      const half8 gm = bitcast<half8>(gs[q]);
       half8 o;
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (_Float16)(((float)h[e] * inv) * (float)gm[e]);
@@ -59,12 +80,35 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
 #pragma unroll
       for (int fi = 0; fi < 4; ++fi) *reinterpret_cast<u32x4*>(base + (size_t)fi * kWave * 8) = f[fi];
     }
+  };
+  if constexpr (kRegs > 0) {
+#pragma unroll
+    for (int i = 0; i < kRegs; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      if (c < nch) emit(c, xv[i], gv[i]);
+    }
+  } else {
+    for (int c = threadIdx.x; c < nch; c += 256) {
+      u32x4 xs[4], gs[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        xs[q] = *reinterpret_cast<const u32x4*>(xr + 32 * c + 8 * q);
+        gs[q] = *reinterpret_cast<const u32x4*>(gamma + 32 * c + 8 * q);
+      }
+      emit(c, xs, gs);
+    }
   }
 }
 
 void launch_rmsnorm(const uint16_t* x, int M, int H, int ldx, const uint16_t* gamma, float eps,
                     uint16_t* out, int ldo, uint16_t* out_prep, hipStream_t st) {
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo, out_prep);
+  const int nch = H / 32;
+  if (nch <= 256)
+    hipLaunchKernelGGL(rmsnorm_kernel<1>, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo, out_prep);
+  else if (nch <= 512)
+    hipLaunchKernelGGL(rmsnorm_kernel<2>, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo, out_prep);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<0>, dim3(M), dim3(256), 0, st, x, H, ldx, gamma, eps, out, ldo, out_prep);
 }
 
 // ---------------------------------------------------------------- KV commit

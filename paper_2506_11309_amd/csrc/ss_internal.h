@@ -100,7 +100,11 @@ void launch_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int n_layers, in
                           int S_max, int D, int32_t* prefix_len, const int32_t* parent, int N, const int32_t* d_last,
                           const int32_t* d_keep, int32_t* new_parent, int32_t* n_kept, int advance, void* ws,
                           hipStream_t st);
-int greedy_accept_splits(int T);  // workgroups per logits row
+int greedy_accept_splits(int T);
+int topk_logprobs_splits(int n);
+size_t topk_logprobs_part_bytes(int n);
+void launch_topk_logprobs(const uint16_t* logits, int ldl, int n, int V, int k, int32_t* tokens, float* logprobs,
+                          void* ws, void* part, hipStream_t st);  // workgroups per logits row
 void launch_greedy_accept(const uint16_t* logits, int ldl, int T, int V, const int32_t* tokens,
                           const int32_t* parent, int32_t* argmax, int32_t* accepted, int32_t* bonus,
                           int32_t* path_len, void* ws, void* part, hipStream_t st);

@@ -208,6 +208,7 @@ const char* swiftspec_status_string(int status) {
     case SWIFTSPEC_WORKSPACE_TOO_SMALL: return "workspace too small";
     case SWIFTSPEC_BAD_TREE: return "invalid parent array";
     case SWIFTSPEC_HIP_ERROR: return "HIP runtime error";
+    case SWIFTSPEC_CAPACITY: return "draft tree capacity exceeded";
     default: return "unknown status";
   }
 }
@@ -514,6 +515,23 @@ int swiftspec_greedy_accept(const uint16_t* logits, int32_t ldl, int32_t T, int3
   if (ws_bytes < swiftspec_greedy_accept_workspace_bytes(T)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   ss::launch_greedy_accept(logits, ldl, T, V, d_tokens, d_parent, d_argmax, d_accepted, d_bonus, d_path_len,
                            ws, static_cast<char*>(ws) + kHeader, S(stream));
+  return check_launch();
+}
+
+size_t swiftspec_topk_logprobs_workspace_bytes(int32_t n) {
+  if (n < 1 || n > SWIFTSPEC_MAX_TREE) return kHeader;
+  return kHeader + align_up(ss::topk_logprobs_part_bytes(n));
+}
+
+int swiftspec_topk_logprobs(const uint16_t* logits, int32_t ldl, int32_t n, int32_t V, int32_t k,
+                            int32_t* d_tokens, float* d_logprobs, void* ws, size_t ws_bytes, void* stream) {
+  if (!logits || !d_tokens || !d_logprobs || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (n < 1 || V < 1 || ldl < V || k < 1 || k > V) return SWIFTSPEC_INVALID_ARG;
+  if (n > SWIFTSPEC_MAX_TREE || k > 8) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(logits) || ldl % 8) return SWIFTSPEC_MISALIGNED;
+  if (ws_bytes < swiftspec_topk_logprobs_workspace_bytes(n)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  ss::launch_topk_logprobs(logits, ldl, n, V, k, d_tokens, d_logprobs, ws, static_cast<char*>(ws) + kHeader,
+                           S(stream));
   return check_launch();
 }
 

@@ -107,6 +107,18 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert reorg(8, D=100) == ss.UNSUPPORTED
     assert reorg(8, stride=100) == ss.INVALID_ARG
     assert reorg(8, last=None) == ss.INVALID_ARG
+    # draft expansion (top-k log-softmax): rows, k, leading dimension, workspace
+    topk = lambda n, V, ldl, k, lg=fake, wsb=1 << 20: lib.swiftspec_topk_logprobs(lg, ldl, n, V, k, fake, fake, fake,
+                                                                                   wsb, None)
+    assert topk(0, 1000, 1000, 4) == ss.INVALID_ARG
+    assert topk(65, 1000, 1000, 4) == ss.UNSUPPORTED
+    assert topk(8, 1000, 1000, 9) == ss.UNSUPPORTED
+    assert topk(8, 1000, 1000, 0) == ss.INVALID_ARG
+    assert topk(8, 4, 8, 5) == ss.INVALID_ARG  # k > V
+    assert topk(8, 1000, 1004, 4) == ss.MISALIGNED
+    assert topk(8, 1000, 1000, 4, lg=fake + 2) == ss.MISALIGNED
+    assert topk(8, 1000, 1000, 4, wsb=16) == ss.WORKSPACE_TOO_SMALL
+    assert lib.swiftspec_topk_logprobs_workspace_bytes(8) >= ss.WS_HEADER_BYTES + 8 * 64 * 9 * 8
 
 
 def test_verify_step_rejects_before_launch(ss):

@@ -328,7 +328,7 @@ def test_w4a16_gemm_rejects_bad_arguments():
 # -------------------------------------------------------------- RMSNorm
 
 
-@pytest.mark.parametrize("M,H", [(1, 2048), (13, 4096), (64, 8192), (3, 96), (2, 16384), (5, 8224)])
+@pytest.mark.parametrize("M,H", [(1, 2048), (13, 4096), (64, 8192), (3, 96), (2, 16384), (5, 8224), (2, 20480)])
 def test_rmsnorm(M, H):
     x = gen.normal_f16(20 + M, 0, (M, H))
     g = gen.normal_f16(21, 0, (H,), 1.0, 0.02)

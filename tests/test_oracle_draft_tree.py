@@ -244,7 +244,9 @@ def test_reroot_off_tree_and_unexpanded_end():
     res = t.reroot([9, 4])
     assert res == {"last": -1, "path_rows": 0, "keep": 0, "pending": [9, 4]}
     with pytest.raises(AssertionError):
-        t.reroot([3])
+        t.reroot([3, 1])
+    with pytest.raises(AssertionError):  # an output holds at least the root and one token
+        t.reroot([4])
 
 
 # ------------------------------------------------------------ top-k

@@ -679,10 +679,12 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
     p.nw = 2;  // one gate and one up tile per wave
     p.nblocks = tiles / 4;
   } else {
-    // above 32 rows two tiles per wave halve the LDS fragment reads per
-    // weight byte, which pays where K is long enough to keep the split-K
-    // partials small
-    p.nw = ((MT <= 2 || K >= 16384) && tiles % 8 == 0) ? 2 : 1;
+    // two tiles per wave halve the LDS fragment reads per weight byte: up
+    // to 32 rows where that still leaves at least 64 blocks and K is long
+    // (the 70B projections; at the 8B widths, 48 and 32 blocks, one tile per
+    // wave is 10-26 % faster, and at K = 2048 15 %), above 32 rows where K
+    // is long enough to keep the split-K partials small
+    p.nw = (((MT <= 2 && tiles / 8 >= 64 && K >= 8192) || K >= 16384) && tiles % 8 == 0) ? 2 : 1;
     p.nblocks = tiles / (4 * p.nw);
   }
   const long units = (long)p.nblocks * (K / 128);
@@ -691,6 +693,10 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
   // at the 70B width: 448 blocks; at 48 and 64 rows 11 % faster than
   // stream-K, whose gate and up partials cost a 16 us fix-up at 64 rows)
   if (swiglu && p.nblocks >= 256 && p.nblocks <= 2 * cap) cap = p.nblocks;
+  // up to 32 rows, about 8 ranges per N-block: more split the blocks into
+  // slivers whose partials the fix-up must sum (1B-shaped projections with
+  // 32 blocks: 12.0 -> 10.6 us at 256 workgroups instead of 512)
+  if (!swiglu && MT <= 2 && 8 * p.nblocks < cap) cap = 8 * p.nblocks;
   p.nwg = (int)(units < cap ? units : cap);
   const int col_w = swiglu ? p.nw / 2 : p.nw;
   const int src = swiglu ? 2 : 1;

@@ -15,12 +15,10 @@
 // expansion step (O(w log s) per step), and per-node tree-cache rows: the
 // root's keys and values are the last prefix row of the draft cache, every
 // other expanded node owns one row, in the order the nodes were selected.
-#include <hip/hip_runtime.h>
-
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
-#include <new>
+#include <utility>
 #include <vector>
 
 #include "../../include/swiftspec.h"
@@ -86,16 +84,27 @@ struct swiftspec_draft_tree {
   int32_t parent_row(int32_t v) const { return parent[v] <= 0 ? -1 : row[parent[v]]; }
 };
 
+// Host allocation failures inside the entry points surface as
+// SWIFTSPEC_CAPACITY; no exception crosses the C ABI.
+#define SS_NOTHROW_BEGIN try {
+#define SS_NOTHROW_END \
+  }                    \
+  catch (...) {        \
+    return SWIFTSPEC_CAPACITY; \
+  }
+
 extern "C" {
 
 int swiftspec_draft_tree_create(int32_t capacity, int32_t root_token, swiftspec_draft_tree** out) {
   if (!out || capacity < 1) return SWIFTSPEC_INVALID_ARG;
   *out = nullptr;
-  swiftspec_draft_tree* t = new (std::nothrow) swiftspec_draft_tree;
-  if (!t) return SWIFTSPEC_CAPACITY;
+  swiftspec_draft_tree* t = nullptr;
+  SS_NOTHROW_BEGIN
+  t = new swiftspec_draft_tree;
   t->capacity = capacity;
   t->token.reserve(capacity);
   t->reset(root_token);
+  SS_NOTHROW_END
   *out = t;
   return SWIFTSPEC_OK;
 }
@@ -159,6 +168,15 @@ int swiftspec_draft_tree_expand(swiftspec_draft_tree* t, int32_t n, const int32_
     }
   }
   if ((int64_t)t->size() + (int64_t)n * k > t->capacity) return SWIFTSPEC_CAPACITY;
+  SS_NOTHROW_BEGIN
+  // make room first, so that the appends below cannot fail half-way
+  const size_t need = (size_t)t->size() + (size_t)n * k;
+  for (auto* v : {&t->token, &t->parent, &t->row, &t->first_child, &t->next_sibling}) v->reserve(need);
+  t->weight.reserve(need);
+  t->expanded.reserve(need);
+  t->selected.reserve(need);
+  t->heap.reserve(t->heap.size() + (size_t)n * k);
+  SS_NOTHROW_END
   for (int32_t j = 0; j < n; ++j) {
     const int32_t v = leaves[j];
     for (int32_t c = 0; c < k; ++c) {
@@ -177,6 +195,7 @@ int swiftspec_draft_tree_select_subgraph(const swiftspec_draft_tree* t, int32_t 
                                          int32_t* parent, int32_t* tokens, int32_t* n) {
   if (!t || bs < 1 || !nodes || !parent || !n) return SWIFTSPEC_INVALID_ARG;
   const int32_t s = t->size(), m = bs < s ? bs : s;
+  SS_NOTHROW_BEGIN
   std::vector<int32_t> all(s);
   for (int32_t v = 0; v < s; ++v) all[v] = v;
   std::nth_element(all.begin(), all.begin() + (m - 1), all.end(),
@@ -190,6 +209,7 @@ int swiftspec_draft_tree_select_subgraph(const swiftspec_draft_tree* t, int32_t 
     parent[j] = v == 0 ? -1 : pos[t->parent[v]];
     if (tokens) tokens[j] = t->token[v];
   }
+  SS_NOTHROW_END
   *n = m;
   return SWIFTSPEC_OK;
 }
@@ -216,6 +236,7 @@ int swiftspec_draft_tree_reroot(swiftspec_draft_tree* t, const int32_t* verified
   *last = last_row;
   *path_rows = rows;
   if (walked == n_verified && end != 0 && t->expanded[end]) {
+    SS_NOTHROW_BEGIN
     // keep end's subtree: nodes in index order, rows in row order
     const int32_t s = t->size();
     std::vector<int32_t> map(s, -1), sub;
@@ -232,24 +253,21 @@ int swiftspec_draft_tree_reroot(swiftspec_draft_tree* t, const int32_t* verified
     std::sort(kept_rows.begin(), kept_rows.end());
     std::vector<int32_t> rowmap(t->n_rows, -1);
     for (size_t j = 0; j < kept_rows.size(); ++j) rowmap[kept_rows[j]] = (int32_t)j;
-    swiftspec_draft_tree old = *t;
-    t->token.clear();
-    t->parent.clear();
-    t->row.clear();
-    t->first_child.clear();
-    t->next_sibling.clear();
-    t->weight.clear();
-    t->expanded.clear();
-    t->selected.clear();
-    const double base = old.weight[end];
+    // built aside and swapped in, so that a failed allocation leaves the tree as it was
+    swiftspec_draft_tree nt;
+    nt.capacity = t->capacity;
+    nt.token.reserve(t->capacity);
+    const double base = t->weight[end];
     for (int32_t v : sub) {
-      const int32_t nv = t->add(old.token[v], v == end ? -1 : map[old.parent[v]], old.weight[v] - base);
-      t->expanded[nv] = old.expanded[v];
-      t->row[nv] = (v == end || old.row[v] < 0) ? -1 : rowmap[old.row[v]];
+      const int32_t nv = nt.add(t->token[v], v == end ? -1 : map[t->parent[v]], t->weight[v] - base);
+      nt.expanded[nv] = t->expanded[v];
+      nt.row[nv] = (v == end || t->row[v] < 0) ? -1 : rowmap[t->row[v]];
     }
-    t->n_rows = (int32_t)kept_rows.size();
-    t->n_selected = 0;
-    t->rebuild_heap();
+    nt.n_rows = (int32_t)kept_rows.size();
+    nt.n_selected = 0;
+    nt.rebuild_heap();
+    std::swap(*t, nt);
+    SS_NOTHROW_END
     *keep = 1;
     *n_pending = 0;
     return SWIFTSPEC_OK;
@@ -260,9 +278,15 @@ int swiftspec_draft_tree_reroot(swiftspec_draft_tree* t, const int32_t* verified
   int32_t np = 0;
   if (!t->expanded[0]) pending[np++] = t->token[0];
   for (int32_t j = 1 + rows; j < n_verified; ++j) pending[np++] = verified[j];
+  SS_NOTHROW_BEGIN
+  swiftspec_draft_tree nt;
+  nt.capacity = t->capacity;
+  nt.token.reserve(t->capacity);
+  nt.reset(verified[n_verified - 1]);
+  std::swap(*t, nt);
+  SS_NOTHROW_END
   *n_pending = np;
   *keep = 0;
-  t->reset(verified[n_verified - 1]);
   return SWIFTSPEC_OK;
 }
 

@@ -50,6 +50,8 @@ def parse():
                     help="skip the one-GPU share of the paper's 70B TP4 kernel benchmarks")
     ap.add_argument("--no-draft-side", action="store_true",
                     help="skip the draft-model kernels (non-square attention, KV reorganisation)")
+    ap.add_argument("--no-tree-loop", action="store_true",
+                    help="skip the sequential tree-generation loop (Alg. 1 with synthetic models)")
     ap.add_argument("--gemm-ab", action="store_true",
                     help="only compare the matrix-core and vector-ALU W4A16 GEMMs over M (JSON line per M)")
     return ap.parse_args()
@@ -263,6 +265,7 @@ def main():
     full = None if args.no_full_step else full_step(args, ss, torch, np, dev, stream)
     draft = None if args.no_draft_side else draft_side(args, ss, torch, np, dev, stream)
     shard = None if args.no_paper_shard else paper_shard(args, ss, torch, np, dev, stream)
+    loop = None if args.no_tree_loop else tree_loop(ss, torch, np, dev, stream)
 
     # ---------------- CPU baseline: the fp64 reference checker ----------------
     cpu = None
@@ -313,6 +316,7 @@ def main():
         "full_step_80_layers": full,
         "draft_side": draft,
         "paper_tp4_shard": shard,
+        "tree_loop": loop,
         "input_generation_s": round(gen_s, 2),
     }
     print(json.dumps(out), flush=True)
@@ -499,6 +503,160 @@ def draft_side(args, ss, torch, np, dev, stream):
             "topk_logprobs_us": round(topk_us, 2),
             "topk_logprobs_gbs": round(w * V * 2 / (topk_us * 1e-6) / 1e9, 1),
             "draft_tree_host": host}
+
+
+def tree_loop(ss, torch, np, dev, stream, V=128256, iters=40, w=8, k=8, d=3, bs=8, p_agree=0.8, seed=2506,
+              check=None):
+    """Iterations of the loop of Alg. 1 run one after the other on one GPU,
+    with synthetic models in place of the draft and target networks.
+
+    The target's greedy choice after a token context is a seeded hash of
+    that context; its logits rows (fp16 N(0, 1), drawn on the device) carry
+    10.0 at that token.  A leaf's draft logits carry 8.0 at the target's
+    choice with probability p_agree (else at a random token), so paths of
+    several tokens get accepted.  Per iteration: d expansion steps (host
+    leaf selection, the leaves' draft rows through the top-k kernel, host
+    expansion; the draft's tree-cache rows are tagged with their tokens),
+    the bs-node subgraph to the target (its rows tagged, the target's
+    logits, greedy acceptance and the KV commit on the device), re-rooting
+    on the output (host) with the draft-cache reorganisation on the device
+    and the pending tokens appended, then growth to bs nodes.  Returns
+    timings (wall clock with the host round trips the loop needs) and the
+    accepted tokens per iteration; `check(state)` is called after every
+    iteration with the host and device state."""
+    import time
+    rng = np.random.default_rng(seed)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    M61 = (1 << 61) - 1
+
+    def push(h, t):  # hash of a context extended by one token
+        return (h * 1000003 + t + 1) % M61
+
+    def choice(h):  # the target's greedy next token after a context
+        return int((h * 0x9E3779B97F4A7C15 >> 17) % V)
+
+    S_max, D, Hkv = 4096, 8, 1
+    P0 = 16
+    committed = [int(t) for t in rng.integers(0, V, P0)]
+    h_prefix = 0
+    for t in committed:
+        h_prefix = push(h_prefix, t)
+    root = int(rng.integers(0, V))
+    tree = ss.DraftTree(1 << 14, root)
+    tk = torch.zeros((Hkv, S_max, D), dtype=torch.int32, device=dev)  # target cache (tags in element 0)
+    dk = torch.zeros((Hkv, S_max, D), dtype=torch.int32, device=dev)  # draft cache
+    tk[0, :P0, 0] = torch.tensor(committed, dtype=torch.int32)
+    dk[0, :P0 + 1, 0] = torch.tensor(committed + [root], dtype=torch.int32)
+    tkv, dkv = tk.view(torch.int16), dk.view(torch.int16)  # the kernels move fp16 rows: 2 x D halves
+    tvv, dvv = torch.zeros_like(tkv), torch.zeros_like(dkv)  # value caches (distinct memory)
+    P_t = torch.tensor([P0], dtype=torch.int32, device=dev)
+    P_d = torch.tensor([P0 + 1], dtype=torch.int32, device=dev)
+    p_d = P0 + 1
+    ws = ss.workspace(1 << 16, dev)
+    ws_k = ss.workspace(ss.topk_logprobs_workspace_bytes(w), dev)
+    ws_a = ss.workspace(ss.greedy_accept_workspace_bytes(bs), dev)
+    d_tok = torch.zeros((w, k), dtype=torch.int32, device=dev)
+    d_lp = torch.zeros((w, k), dtype=torch.float32, device=dev)
+    d_am = torch.zeros(bs, dtype=torch.int32, device=dev)
+    d_acc, d_bonus, d_len = (torch.zeros(1, dtype=torch.int32, device=dev) for _ in range(3))
+    t_draft = t_target = t_reroot = 0.0
+    n_steps = 0
+    accepted = []
+
+    def node_hashes():
+        tok, par, _, row, _ = tree.nodes()
+        hs = [0] * len(tok)
+        for v in range(len(tok)):  # parents precede children
+            hs[v] = push(h_prefix, int(tok[v])) if v == 0 else push(hs[par[v]], int(tok[v]))
+        return tok, par, row, hs
+
+    def expand_step():
+        leaves, _ = tree.select_leaves(w)
+        n = len(leaves)
+        if n == 0:
+            return
+        tok, par, row, hs = node_hashes()
+        for v in leaves:
+            if v != 0:
+                dk[0, p_d + int(row[v]), 0] = int(tok[v])
+        lg = torch.randn((n, V), generator=gen, device=dev).half()
+        agree = rng.random(n) < p_agree
+        cols = [choice(hs[v]) if agree[j] else int(rng.integers(0, V)) for j, v in enumerate(leaves)]
+        lg[torch.arange(n, device=dev), torch.tensor(cols, device=dev)] = 8.0
+        ss.topk_logprobs(lg.view(torch.int16), d_tok[:n], d_lp[:n], ws_k, stream=stream)
+        tree.expand(leaves, d_tok[:n].cpu().numpy(), d_lp[:n].cpu().numpy())
+
+    with torch.cuda.stream(stream):
+        for it in range(iters):
+            t0 = time.perf_counter()
+            for _ in range(d):
+                if tree.rows() + w <= 64:
+                    expand_step()
+                    n_steps += 1
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            # ---- target: verify the bs most probable nodes ----
+            nodes, par, toks = tree.select_subgraph(bs)
+            T = len(nodes)
+            _, _, _, hs = node_hashes()
+            p_t = int(P_t.item())
+            tk[0, p_t:p_t + T, 0] = torch.from_numpy(toks.astype(np.int32)).to(dev)  # the tree's new rows
+            lg_t = torch.randn((T, V), generator=gen, device=dev).half()
+            lg_t[torch.arange(T, device=dev), torch.tensor([choice(hs[v]) for v in nodes], device=dev)] = 10.0
+            d_par = torch.from_numpy(par.astype(np.int32)).to(dev)
+            d_toks = torch.from_numpy(toks.astype(np.int32)).to(dev)
+            ss.greedy_accept(lg_t.view(torch.int16), d_toks, d_par, d_am[:T], d_acc, d_bonus, ws_a,
+                             path_len=d_len, stream=stream)
+            ss.kv_commit(tkv, tvv, P_t, d_par, d_acc, advance=True, ws=ws, stream=stream)
+            a, b, L = int(d_acc.item()), int(d_bonus.item()), int(d_len.item())
+            path = []
+            j = a
+            while j >= 0:
+                path.append(int(toks[j]))
+                j = int(par[j])
+            path = path[::-1]
+            t2 = time.perf_counter()
+            # ---- draft: re-root on the output, reorganise its cache ----
+            forest = tree.forest()
+            res = tree.reroot(path + [b])
+            if len(forest) > 0:
+                d_f = torch.from_numpy(forest.astype(np.int32)).to(dev)
+                d_last = torch.tensor([res["last"]], dtype=torch.int32, device=dev)
+                d_keep = torch.tensor([res["keep"]], dtype=torch.int32, device=dev)
+                ss.kv_reorganize(dkv, dvv, P_d, d_f, d_last, d_keep, advance=True, ws=ws, stream=stream)
+            p_d += res["path_rows"]
+            for t in res["pending"]:
+                dk[0, p_d, 0] = t
+                p_d += 1
+            P_d.fill_(p_d)
+            committed += path
+            for t in path:
+                h_prefix = push(h_prefix, t)
+            while tree.size() < bs and tree.rows() + w <= 64:
+                expand_step()
+                n_steps += 1
+            torch.cuda.synchronize()
+            t3 = time.perf_counter()
+            t_draft += t1 - t0
+            t_target += t2 - t1
+            t_reroot += t3 - t2
+            accepted.append(L)
+            if check is not None:
+                check({"it": it, "committed": committed, "bonus": b, "path": path, "L": L, "logits": lg_t,
+                       "tokens": toks, "parent": par, "argmax": d_am[:T].cpu().numpy(), "accepted": a,
+                       "P_t": int(P_t.item()), "p_d": p_d, "tk": tk, "dk": dk, "tree": tree, "res": res})
+    if ss.read_device_error(ws, stream):
+        raise RuntimeError("device error in the tree loop")
+    return {"workload": f"sequential loop of Alg. 1 on one GPU, synthetic draft and target (V={V}, "
+                        f"w={w}, k={k}, d={d}, bs={bs}, draft agrees with the target w.p. {p_agree})",
+            "iterations": iters,
+            "mean_accepted_per_iteration": round(float(np.mean(accepted)), 2),
+            "draft_expansion_ms_per_iteration": round(t_draft / iters * 1e3, 3),
+            "verify_accept_commit_ms_per_iteration": round(t_target / iters * 1e3, 3),
+            "reroot_reorganise_grow_ms_per_iteration": round(t_reroot / iters * 1e3, 3),
+            "expansion_steps": n_steps,
+            "note": "wall clock with the host round trips of a Python driver; no target or draft network runs"}
 
 
 def draft_tree_host(ss, np, w=8, k=8, d=3, bs=8, iters=200, vocab=128256):

@@ -62,7 +62,7 @@ def _run(lg, V, k, ws=None):
 
 
 @pytest.mark.parametrize("n,V,k,pad", [(8, 128256, 8, 0), (1, 1000, 1, 1), (64, 32000, 8, 0), (3, 77, 5, 2),
-                                       (5, 4099, 8, 0), (2, 9, 8, 0), (17, 128256, 3, 1)])
+                                       (5, 4099, 8, 0), (2, 9, 8, 0), (17, 128256, 3, 1), (2, 150001, 8, 1)])
 def test_topk_matches_oracle(n, V, k, pad):
     lg = _logits(n, V, pad, seed=n * 1000 + V)
     tok, lp, ws = _run(lg, V, k)

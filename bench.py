@@ -93,8 +93,8 @@ def read_traffic(kernel_tag, cur_hash):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU path "
-              "is not part of this build.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); sharding across GPUs "
+              "is not implemented.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch

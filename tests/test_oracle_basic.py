@@ -290,3 +290,38 @@ def test_rope_scores_depend_only_on_relative_position():
     base = oracle.rope(q, 10) @ oracle.rope(k, 3)
     for shift in (1, 100, 4000):
         assert abs(oracle.rope(q, 10 + shift) @ oracle.rope(k, 3 + shift) - base) < 1e-9
+
+
+# ---------------------------------------------------------------- LM head
+
+
+def test_lm_head_matches_numpy_on_a_non_square_head():
+    # logits = fp16(fp16(rmsnorm(h) * gamma) @ W^T) with W stored [V][H]: a
+    # head read as [H][V], or a skipped normalisation, changes every value
+    M, H, V = 5, 256, 48
+    h = gen.normal_f16(44, 0, (M, H), 0.0, 3.0)
+    gamma = gen.normal_f16(45, 0, (H,), 1.0, 0.02)
+    W = gen.normal_f16(46, 0, (V, H), 0.0, 0.02)
+    hf = h.view(np.float16).astype(np.float64)
+    xn = hf / np.sqrt((hf * hf).mean(axis=1, keepdims=True) + 1e-5) * gamma.view(np.float16).astype(np.float64)
+    xn16 = xn.astype(np.float16).astype(np.float64)
+    ref = _np_f16_bits(xn16 @ W.view(np.float16).astype(np.float64).T)
+    got = oracle.lm_head(h, gamma, W)
+    assert got.shape == (M, V)
+    diff = np.abs(got.astype(np.int32) - ref.astype(np.int32))
+    assert diff.max() <= 1 and (diff == 0).mean() > 0.95
+
+
+def test_lm_head_one_hot_row_reads_one_column_of_the_head():
+    # a row a * e_k normalises to c * e_k, c = fp16(a / sqrt(a^2 / H + eps))
+    # (gamma = 1), so its logits are exactly fp16(c * W[:, k])
+    H, V = 256, 40
+    W = gen.normal_f16(47, 0, (V, H), 0.0, 0.5)
+    gamma = np.full(H, 1.0, np.float16).view(np.uint16)
+    wf = W.view(np.float16).astype(np.float64)
+    for k, a in ((0, 1.0), (37, -2.5), (255, 0.75)):
+        h = np.zeros((1, H), np.float16)
+        h[0, k] = a
+        c = np.float64(np.float16(a / np.sqrt(a * a / H + 1e-5)))
+        got = oracle.lm_head(h.view(np.uint16), gamma, W)
+        assert np.array_equal(got[0], _np_f16_bits(c * wf[:, k]))

@@ -264,8 +264,10 @@ int swiftspec_draft_tree_attention(const uint16_t* q, int32_t ldq, const uint16_
  * (nullable) = S.  If advance != 0, *d_prefix_len becomes P + L after the
  * copy (stream-ordered).  With *d_keep == 0 and a single-root tree this is
  * swiftspec_kv_commit.  1 <= N <= 64, D % 8 == 0, D <= 256, caches 16-byte
- * aligned.  Invalid device data (forest, last, prefix) sets the error word
- * (ws may be NULL: then it is not reported) and nothing is written. */
+ * aligned.  d_new_parent must not overlap d_parent[0 .. N) (the old forest
+ * is read while the new one is written): SWIFTSPEC_INVALID_ARG.  Invalid
+ * device data (forest, last, prefix) sets the error word (ws may be NULL:
+ * then it is not reported) and nothing is written. */
 int swiftspec_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_layers, int64_t layer_stride_elems,
                             int32_t Hkv, int32_t S_max, int32_t D, int32_t* d_prefix_len, const int32_t* d_parent,
                             int32_t N, const int32_t* d_last, const int32_t* d_keep, int32_t* d_new_parent,

@@ -198,20 +198,16 @@ __global__ __launch_bounds__(256) void topk_logprobs_kernel(TopkArgs a) {
       wsum = s_s[lane];
     }
     butterfly_merge(W, wm, wsum, 16);  // lanes 0..15 (4..15 empty) all end with the result
-    // lane r < kTopK publishes entry r, lane kTopK the normaliser
-    const size_t slot = (size_t)row * a.S + sp;
-    if (lane < kTopK) {
-      uint64_t key = W[0];
+    // lane 0 (which holds the whole list, like every lane) publishes the
+    // entries and the normaliser and takes the ticket, so that the ticket's
+    // release covers every store of the partial
+    if (lane == 0) {
+      const size_t slot = (size_t)row * a.S + sp;
 #pragma unroll
-      for (int r = 1; r < kTopK; ++r)
-        if (lane == r) key = W[r];
-      __hip_atomic_store(a.part + slot * kTopK + lane, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else if (lane == kTopK) {
+      for (int r = 0; r < kTopK; ++r)
+        __hip_atomic_store(a.part + slot * kTopK + r, W[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(a.stats + slot, ((uint64_t)__float_as_uint(wsum) << 32) | __float_as_uint(wm),
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    wait_all_memory();  // the wave's stores are complete before its ticket
-    if (lane == 0) {
       uint32_t* row_counter = ws_counters(a.ws) + 16 * (1 + row);  // 64 bytes apart
       const bool last = take_ticket(row_counter) == (uint32_t)(a.S - 1);
       if (last) reset_counter(row_counter);  // for the next launch (stream-ordered)

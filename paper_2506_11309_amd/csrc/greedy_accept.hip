@@ -111,7 +111,6 @@ __global__ __launch_bounds__(256) void greedy_accept_kernel(AcceptArgs a) {
       }
     __hip_atomic_store(a.part + blockIdx.x, ((uint64_t)(uint32_t)bi << 32) | __float_as_uint(bv), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
-    wait_all_memory();
     // tickets in two levels, so that no counter takes more than max(S, T)
     // atomics: the last workgroup of a row combines the row, the last row
     // to finish walks the tree
@@ -133,7 +132,6 @@ __global__ __launch_bounds__(256) void greedy_accept_kernel(AcceptArgs a) {
       }
       // a row of NaNs alone keeps the sentinel: report index 0
       __hip_atomic_store(a.argmax + row, ci < a.V ? ci : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      wait_all_memory();
       last = take_ticket(ws_counters(a.ws)) == (uint32_t)(a.T - 1);
     }
     s_ticket = last;

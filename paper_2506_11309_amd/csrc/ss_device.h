@@ -126,8 +126,6 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Wait until every outstanding memory operation of this wave has completed
-// (stores acknowledged at their coherence scope).
 // Raw buffer resource over [p, p + bytes) (stride 0; dword 3 = the CDNA
 // raw-buffer format), and 16- / 4-byte loads at voffset + soffset from it.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint32_t bytes) {
@@ -140,12 +138,15 @@ __device__ __forceinline__ uint32_t buffer_load_x1(__amdgpu_buffer_rsrc_t r, uin
   return __builtin_amdgcn_raw_buffer_load_b32(r, voffset, soffset, 0);
 }
 
-__device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
-
-// Ticket for the deterministic "last arriving workgroup combines" pattern.
-// Called by one lane after the workgroup's partial stores completed.
+// Ticket for the deterministic "last arriving workgroup combines" pattern,
+// taken by the lane that stored the workgroup's partial.  Acquire-release at
+// agent scope: the release publishes that lane's earlier stores (every
+// later ticket holder reads the counter through the release sequence of
+// these read-modify-writes), and the acquire lets the last holder read
+// every earlier holder's stores; other lanes of the last workgroup read
+// them after a workgroup barrier that follows the ticket.
 __device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
-  return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void reset_counter(uint32_t* counter) {
   __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -161,48 +162,36 @@ namespace ss {
 // fetches each MFMA A-fragment with one coalesced 16-byte load per lane.
 // Lane kq*16 + (m % 16) of fragment f holds 8 values of row m from k-range
 // [128 g + 32 kq, +32), in the slot order the int4 dequantisation produces:
-// fragments 0/1 take the even k of that range (first/second 16), stored
-// multiplied by 16 (exact), fragments 2/3 the odd k.  Within a fragment the
-// order is 0,4,2,6,8,12,10,14 (+1 for odd k).
-__host__ __device__ inline size_t prep_offset(int m, int k, int G, bool* lo) {
+// fragments 0/1 take the even k of that range (first/second 16), fragments
+// 2/3 the odd k.  Within a fragment the order is 0,4,2,6,8,12,10,14 (+1 for
+// odd k).  Values are stored unchanged, so every fp16 input is accepted.
+__host__ __device__ inline size_t prep_offset(int m, int k, int G) {
   const int mt = m >> 4, r16 = m & 15, g = k >> 7, j = k & 127, kq = j >> 5, t = j & 31;
   const int f = ((t & 1) << 1) | (t >> 4);
   const int u = (t & 15) >> 1;
   const int e = (u & 4) | ((u & 1) << 1) | ((u >> 1) & 1);
-  *lo = (t & 1) == 0;
   return ((((size_t)mt * G + g) * 4 + f) * 64 + (kq * 16 + r16)) * 8 + e;
 }
 
 // Store the fp16 value h of activation (m, k) into a prepared buffer.
 __device__ __forceinline__ void store_prepared(uint16_t* prep, int m, int k, int G, uint16_t h) {
-  bool lo;
-  const size_t off = prep_offset(m, k, G, &lo);
-  if (lo) {
-    _Float16 v;
-    __builtin_memcpy(&v, &h, 2);
-    v = v * (_Float16)16.0f;  // exact scaling by a power of two
-    __builtin_memcpy(&h, &v, 2);
-  }
-  prep[off] = h;
+  prep[prep_offset(m, k, G)] = h;
 }
 
 // Prepared-layout fragments of 32 consecutive activations k = 128 g + 32 kq
 // + t, t = 0..31, of one row, given as 16 u32 (element t in half t % 2 of
-// word t / 2): fragment 0 holds even t < 16, 1 even t >= 16 (both x 16), 2
-// odd t < 16, 3 odd t >= 16, each in slot order u = 0, 2, 1, 3, 4, 6, 5, 7
-// of u = (t % 16) / 2 -- the order prep_offset describes.  They belong at
+// word t / 2): fragment 0 holds even t < 16, 1 even t >= 16, 2 odd t < 16,
+// 3 odd t >= 16, each in slot order u = 0, 2, 1, 3, 4, 6, 5, 7 of
+// u = (t % 16) / 2 -- the order prep_offset describes.  They belong at
 // ((((m / 16) * G + g) * 4 + f) * 64 + kq * 16 + m % 16) * 8 halves.
 __device__ __forceinline__ void pack_prepared(const uint32_t (&a)[16], u32x4 (&f)[4]) {
-  const _Float16 sixteen = (_Float16)16.0f;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const uint32_t* b = a + 8 * h;
-    const u32x4 lo = {(b[0] & 0xFFFFu) | (b[2] << 16), (b[1] & 0xFFFFu) | (b[3] << 16),
-                      (b[4] & 0xFFFFu) | (b[6] << 16), (b[5] & 0xFFFFu) | (b[7] << 16)};
-    const u32x4 hi = {(b[0] >> 16) | (b[2] & 0xFFFF0000u), (b[1] >> 16) | (b[3] & 0xFFFF0000u),
-                      (b[4] >> 16) | (b[6] & 0xFFFF0000u), (b[5] >> 16) | (b[7] & 0xFFFF0000u)};
-    f[h] = bitcast<u32x4>(bitcast<half8>(lo) * sixteen);
-    f[2 + h] = hi;
+    f[h] = u32x4{(b[0] & 0xFFFFu) | (b[2] << 16), (b[1] & 0xFFFFu) | (b[3] << 16),
+                 (b[4] & 0xFFFFu) | (b[6] << 16), (b[5] & 0xFFFFu) | (b[7] << 16)};
+    f[2 + h] = u32x4{(b[0] >> 16) | (b[2] & 0xFFFF0000u), (b[1] >> 16) | (b[3] & 0xFFFF0000u),
+                     (b[4] >> 16) | (b[6] & 0xFFFF0000u), (b[5] >> 16) | (b[7] & 0xFFFF0000u)};
   }
 }
 

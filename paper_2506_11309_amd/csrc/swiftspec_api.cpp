@@ -488,6 +488,11 @@ int swiftspec_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int32_t n_laye
                             int32_t* d_n_kept, int32_t advance, void* ws, size_t ws_bytes, void* stream) {
   if (!k_cache || !v_cache || !d_prefix_len || !d_parent || !d_last || !d_keep) return SWIFTSPEC_INVALID_ARG;
   if (n_layers < 1 || Hkv < 1 || N < 1 || S_max < N || D < 8) return SWIFTSPEC_INVALID_ARG;
+  if (d_new_parent) {  // the old forest is read while the new one is written
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(d_parent), b0 = reinterpret_cast<uintptr_t>(d_new_parent);
+    const uintptr_t bytes = (uintptr_t)N * sizeof(int32_t);
+    if (a0 < b0 + bytes && b0 < a0 + bytes) return SWIFTSPEC_INVALID_ARG;
+  }
   if (layer_stride_elems < (int64_t)Hkv * S_max * D) return SWIFTSPEC_INVALID_ARG;
   if (N > SWIFTSPEC_MAX_TREE || D % 8 || D > 256) return SWIFTSPEC_UNSUPPORTED;
   if (!aligned16(k_cache) || !aligned16(v_cache) || layer_stride_elems % 8) return SWIFTSPEC_MISALIGNED;

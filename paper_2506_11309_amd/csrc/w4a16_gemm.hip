@@ -12,16 +12,14 @@
 //   * Lane (n = lane % 16, kq = lane / 16) loads 16 bytes = k in
 //     [128 g + 32 kq, +32) of weight row n: one wave-wide load covers one
 //     16-column x 128-k block, i.e. exactly one (scale, zero) group.
-//   * Dequantisation to exact integers with the fp16 "magic number" 1024:
-//     OR-ing a nibble field into 0x6400 gives 1024 + q (low nibble) or
-//     1024 + 16 q (high nibble), and one packed fp16 subtraction of 1024 + z
-//     (1024 + 16 z) leaves q - z (16 (q - z)) exactly.  Low-nibble slots
-//     meet activations pre-multiplied by 16, so every product is
-//     16 x (q - z) exactly and the MFMA sum of a group is
-//     C_g = 16 sum_k x (q - z).  Per group the accumulator takes s C_g (one
-//     mixed-precision FMA per output element, fp16 s read in place), and
-//     the block's sum is multiplied by 1/16 once at its end (exact: a power
-//     of two), which equals summing (s / 16) C_g.
+//   * Dequantisation to exact integers with fp16 "magic numbers": OR-ing the
+//     low nibble field into 0x6400 (1024, unit 1) gives 1024 + q, OR-ing the
+//     high nibble field (bits 4-7) into 0x5400 (64, unit 1/16) gives 64 + q,
+//     and one packed fp16 subtraction of 1024 + z (64 + z) leaves q - z
+//     exactly.  Activations are used as given (any fp16 value), each MFMA
+//     sum of a group is C_g = sum_k x (q - z), and the accumulator takes
+//     s C_g (one mixed-precision FMA per output element, fp16 s read in
+//     place).
 //   * Stream-K scheduling: a fixed grid of workgroups (4 waves each) splits
 //     the (N-block, group) iteration space into equal contiguous ranges; the
 //     4 waves split an N-block's columns.  Per group, every wave loads 1 KB
@@ -249,16 +247,16 @@ void w4a16_gemm_kernel(GemmArgs a) {
     for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Dequantisation to exact small integers: (w & 0x000F000F) | 0x64006400
-  // is the fp16 pair (1024 + q, 1024 + q'), (w & 0x00F000F0) | 0x64006400 is
-  // (1024 + 16 q, ...); subtracting 1024 + z (resp. 1024 + 16 z) leaves
-  // q - z (resp. 16 (q - z)) exactly.  Low-nibble slots meet activations
-  // pre-multiplied by 16, so the MFMA sum of a group is C_g = 16 sum_k x (q - z)
-  // and the accumulator takes s C_g (scaled by 1/16 when the block ends).
-  // The magic constant is kept in a register (opaque to the optimiser) so
-  // that mask-and-insert is one v_bfi_b32 with the mask in a scalar register.
-  uint32_t magic = 0x64006400u;
-  asm volatile("" : "+v"(magic));
-  auto deq = [&](uint32_t x, uint32_t m, half2v zz) {
+  // is the fp16 pair (1024 + q, 1024 + q'), (w & 0x00F000F0) | 0x54005400 is
+  // (64 + q, 64 + q') (the nibble sits at the 1/16 ... 1/2 mantissa bits of
+  // 64, i.e. at units 1 ... 8); subtracting 1024 + z (resp. 64 + z) leaves
+  // q - z exactly.  The MFMA sum of a group is C_g = sum_k x (q - z) and the
+  // accumulator takes s C_g.  The magic constants are kept in registers
+  // (opaque to the optimiser) so that mask-and-insert is one v_bfi_b32 with
+  // the mask in a scalar register.
+  uint32_t magic_lo = 0x64006400u, magic_hi = 0x54005400u;
+  asm volatile("" : "+v"(magic_lo), "+v"(magic_hi));
+  auto deq = [&](uint32_t x, uint32_t m, uint32_t magic, half2v zz) {
     return bitcast<uint32_t>(bitcast<half2v>((x & m) | (magic & ~m)) - zz);
   };
   auto read_a = [&](int slot, half8 (&af)[MT][4]) {
@@ -279,11 +277,13 @@ void w4a16_gemm_kernel(GemmArgs a) {
       constexpr uint32_t kLo = 0x000F000Fu, kHi = 0x00F000F0u;
       const uint32_t z = (st.sz[nt] >> 16) & 0xFFu;
       const half2v zlo = bitcast<half2v>((0x6400u + z) * 0x00010001u);
-      const half2v zhi = bitcast<half2v>((0x6400u + 16u * z) * 0x00010001u);
-      const half8 blo_a = bitcast<half8>(u32x4{deq(w[0], kLo, zlo), deq(s0, kLo, zlo), deq(w[1], kLo, zlo), deq(s1, kLo, zlo)});
-      const half8 blo_b = bitcast<half8>(u32x4{deq(w[2], kLo, zlo), deq(s2, kLo, zlo), deq(w[3], kLo, zlo), deq(s3, kLo, zlo)});
-      const half8 bhi_a = bitcast<half8>(u32x4{deq(w[0], kHi, zhi), deq(s0, kHi, zhi), deq(w[1], kHi, zhi), deq(s1, kHi, zhi)});
-      const half8 bhi_b = bitcast<half8>(u32x4{deq(w[2], kHi, zhi), deq(s2, kHi, zhi), deq(w[3], kHi, zhi), deq(s3, kHi, zhi)});
+      const half2v zhi = bitcast<half2v>((0x5400u + 16u * z) * 0x00010001u);
+      auto dl = [&](uint32_t x) { return deq(x, kLo, magic_lo, zlo); };
+      auto dh = [&](uint32_t x) { return deq(x, kHi, magic_hi, zhi); };
+      const half8 blo_a = bitcast<half8>(u32x4{dl(w[0]), dl(s0), dl(w[1]), dl(s1)});
+      const half8 blo_b = bitcast<half8>(u32x4{dl(w[2]), dl(s2), dl(w[3]), dl(s3)});
+      const half8 bhi_a = bitcast<half8>(u32x4{dh(w[0]), dh(s0), dh(w[1]), dh(s1)});
+      const half8 bhi_b = bitcast<half8>(u32x4{dh(w[2]), dh(s2), dh(w[3]), dh(s3)});
       sw[nt] = st.sz[nt];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
@@ -321,10 +321,6 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // range holds the whole N-block, else publish the partial (slot 0: the
   // range's first N-block, slot 1: its last) for the fix-up kernel.
   auto flush = [&](int nb) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] *= 0.0625f;  // the 16 of C_g, exactly
     const bool full = (long)nb * G >= u_lo && (long)(nb + 1) * G <= u_hi;
     if constexpr (kSplit) {
       // every range holds whole blocks: the up waves hand their sums to the

@@ -10,7 +10,7 @@
 // waves of one tile share its weight block through the caches); lane
 // (n = lane % 16, kq = lane / 16) dequantises its 32 nibbles of column n
 // (k in [128 g + 32 kq, +32)) to 16 fp16 pairs of exact integers (magic
-// number 1024, as in the matrix-core kernel), and for each of its 16 token
+// numbers 1024 and 64, as in the matrix-core kernel), and for each of its 16 token
 // rows forms the 32-term dot product with v_dot2_f32_f16 (16 instructions per
 // row and group) against the row's four activation fragments, which the
 // workgroup stages through a 3-slot LDS ring (lanes of one kq read the same
@@ -69,9 +69,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void w
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) abuf[slot][mt][wave][lane] = r[mt];
   };
-  uint32_t magic = 0x64006400u;
-  asm volatile("" : "+v"(magic));
-  auto deq = [&](uint32_t x, uint32_t m, half2v zz) {
+  // exact dequantisation as in the matrix-core GEMM: low nibbles in 0x6400
+  // (1024 + q), high nibbles (bits 4-7) in 0x5400 (64 + q), minus 1024 + z
+  // resp. 64 + z
+  uint32_t magic_lo = 0x64006400u, magic_hi = 0x54005400u;
+  asm volatile("" : "+v"(magic_lo), "+v"(magic_hi));
+  auto deq = [&](uint32_t x, uint32_t m, uint32_t magic, half2v zz) {
     return bitcast<half2v>(bitcast<half2v>((x & m) | (magic & ~m)) - zz);
   };
 
@@ -84,13 +87,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void w
     constexpr uint32_t kLo = 0x000F000Fu, kHi = 0x00F000F0u;
     const uint32_t z = (sz >> 16) & 0xFFu;
     const half2v zlo = bitcast<half2v>((0x6400u + z) * 0x00010001u);
-    const half2v zhi = bitcast<half2v>((0x6400u + 16u * z) * 0x00010001u);
+    const half2v zhi = bitcast<half2v>((0x5400u + 16u * z) * 0x00010001u);
+    auto dl = [&](uint32_t x) { return deq(x, kLo, magic_lo, zlo); };
+    auto dh = [&](uint32_t x) { return deq(x, kHi, magic_hi, zhi); };
     // B pairs in the element order of the four activation fragments
-    const half2v b[16] = {deq(w[0], kLo, zlo), deq(s0, kLo, zlo), deq(w[1], kLo, zlo), deq(s1, kLo, zlo),
-                          deq(w[2], kLo, zlo), deq(s2, kLo, zlo), deq(w[3], kLo, zlo), deq(s3, kLo, zlo),
-                          deq(w[0], kHi, zhi), deq(s0, kHi, zhi), deq(w[1], kHi, zhi), deq(s1, kHi, zhi),
-                          deq(w[2], kHi, zhi), deq(s2, kHi, zhi), deq(w[3], kHi, zhi), deq(s3, kHi, zhi)};
-    const float s16 = h2f((uint16_t)(sz & 0xFFFFu)) * 0.0625f;
+    const half2v b[16] = {dl(w[0]), dl(s0), dl(w[1]), dl(s1), dl(w[2]), dl(s2), dl(w[3]), dl(s3),
+                          dh(w[0]), dh(s0), dh(w[1]), dh(s1), dh(w[2]), dh(s2), dh(w[3]), dh(s3)};
+    const float sc = h2f((uint16_t)(sz & 0xFFFFu));
     // fragment f of row r at xb[f * 64 + r].  The base is passed through an
     // empty asm that depends on the row two before, so that the compiler
     // keeps at most two rows' fragment reads (16 registers each) in flight
@@ -107,7 +110,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void w
 #pragma unroll
         for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_fdot2(bitcast<half2v>(xv[e]), b[4 * f + e], c, false);
       }
-      acc[r] = __builtin_fmaf(c, s16, acc[r]);
+      acc[r] = __builtin_fmaf(c, sc, acc[r]);
     }
   };
 

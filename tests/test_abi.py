@@ -107,6 +107,12 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert reorg(8, D=100) == ss.UNSUPPORTED
     assert reorg(8, stride=100) == ss.INVALID_ARG
     assert reorg(8, last=None) == ss.INVALID_ARG
+    # the renumbered forest may not be written over the forest being read
+    alias = lambda par, newp: lib.swiftspec_kv_reorganize(fake, fake, 2, 8 * 200 * 128, 8, 200, 128, fake, par, 8,
+                                                          fake, fake, newp, None, 0, None, 0, None)
+    assert alias(fake, fake) == ss.INVALID_ARG
+    assert alias(fake, fake + 16) == ss.INVALID_ARG  # overlaps d_parent[4 .. 8)
+    assert alias(fake + 16, fake) == ss.INVALID_ARG
     # draft expansion (top-k log-softmax): rows, k, leading dimension, workspace
     topk = lambda n, V, ldl, k, lg=fake, wsb=1 << 20: lib.swiftspec_topk_logprobs(lg, ldl, n, V, k, fake, fake, fake,
                                                                                    wsb, None)

@@ -470,8 +470,6 @@ def test_prepared_activation_layout_is_bit_exact():
             for f in range(4):
                 base = k0 + 16 * (f % 2) + (f // 2)  # even k for f < 2, odd k for f >= 2
                 vals = np.array([xf[m, base + o] for o in order], np.float16)
-                if f < 2:
-                    vals = (vals.astype(np.float32) * 16).astype(np.float16)
                 exp[m // 16, g, f, lane] = vals.view(np.uint16)
     assert np.array_equal(got.reshape(exp.shape), exp)
 

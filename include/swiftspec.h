@@ -189,6 +189,28 @@ int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, 
                              int32_t Hq, int32_t Hkv, int32_t D, const float* rope_cos_sin,
                              float softmax_scale, uint16_t* out, int32_t ldo, void* ws,
                              size_t ws_bytes, void* stream);
+/* Tree attention that allocates nothing, for callers that cannot allocate
+ * device memory or hand over a workspace (work under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments
+ * and results as swiftspec_tree_attention, without ws / ws_bytes: the split
+ * partials live in a library-owned device array of
+ * SWIFTSPEC_NOALLOC_SCRATCH_BYTES on each GPU the library runs on, held
+ * until the process ends; nothing in it needs to start at zero.  d_error
+ * (device uint32, nullable) receives the device error bits
+ * (SWIFTSPEC_DEVERR_*, OR-ed in; the caller clears it).  A shape whose
+ * partials do not fit returns SWIFTSPEC_WORKSPACE_TOO_SMALL before any
+ * launch (the Llama-3 1B/8B/70B shapes at T <= 64 need at most 8.5 MB).
+ * The first call on a device looks up the array's device address
+ * (SWIFTSPEC_HIP_ERROR if that fails).  No call allocates or frees memory.
+ * Every call on one GPU shares its array: calls that overlap in time on one
+ * GPU (several streams or threads) race, and their results are undefined. */
+#define SWIFTSPEC_NOALLOC_SCRATCH_BYTES (16u << 20)
+int swiftspec_tree_attention_noalloc(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                                     int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
+                                     const int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,
+                                     int32_t Hq, int32_t Hkv, int32_t D, const float* rope_cos_sin,
+                                     float softmax_scale, uint16_t* out, int32_t ldo, uint32_t* d_error,
+                                     void* stream);
 size_t swiftspec_tree_attention_workspace_bytes(int32_t T, int32_t Hq, int32_t Hkv, int32_t D,
                                                 int32_t S_max);
 

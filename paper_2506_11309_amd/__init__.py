@@ -93,6 +93,8 @@ _SIGS = {
     "swiftspec_tree_attention": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, f32,
                                   vp, i32, vp, sz, vp], ctypes.c_int),
     "swiftspec_tree_attention_workspace_bytes": ([i32, i32, i32, i32, i32], sz),
+    "swiftspec_tree_attention_noalloc": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, f32,
+                                          vp, i32, vp, vp], ctypes.c_int),
     "swiftspec_rope_table": ([f64, i32, i32, vp], ctypes.c_int),
     "swiftspec_tree_masks": ([vp, i32, i32, vp, vp, vp, vp], ctypes.c_int),
     "swiftspec_tree_validate": ([vp, i32, vp], ctypes.c_int),
@@ -303,6 +305,25 @@ def tree_attention(q, k, v, k_cache, v_cache, prefix_len, parent, Hq, Hkv, D, ro
                                           _ptr(out), out.stride(0), _ptr(ws), ws.numel(),
                                           _stream(stream))
     _check(st, "tree_attention")
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def tree_attention_noalloc(q, k, v, k_cache, v_cache, prefix_len, parent, Hq, Hkv, D, rope, out, error=None,
+                           softmax_scale=None, stream=None):
+    """tree_attention without a workspace (partials in the library's own
+    device array); error: device int32[1] that receives the device error
+    bits, or None."""
+    T = parent.shape[0]
+    S_max = k_cache.shape[-2]
+    if softmax_scale is None:
+        softmax_scale = 1.0 / (D ** 0.5)
+    st = _load().swiftspec_tree_attention_noalloc(_ptr(q), q.stride(0), _ptr(k), _ptr(v), k.stride(0),
+                                                  _ptr(k_cache), _ptr(v_cache), S_max, _ptr(prefix_len),
+                                                  _ptr(parent), T, Hq, Hkv, D, _ptr(rope), softmax_scale,
+                                                  _ptr(out), out.stride(0), _ptr(error), _stream(stream))
+    _check(st, "tree_attention_noalloc")
 
 
 def tree_masks(parents, anc, depth, status, stream=None):

@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "../../include/swiftspec.h"
@@ -157,6 +158,36 @@ void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t
   L.nsplit = p.nsplit;
   L.chunk = p.chunk;
   ss::launch_tree_attention(L, st);
+}
+
+// ---- tree attention without allocation: partials in a library-owned array
+// of SWIFTSPEC_NOALLOC_SCRATCH_BYTES per GPU.  In host code `scratch` names a
+// host-side stand-in; the device address of each GPU's copy is looked up
+// once per device (with that device current) and used everywhere instead.
+static __device__ __align__(256) unsigned char scratch[SWIFTSPEC_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, or nullptr with the
+// status in *rc.
+void* noalloc_scratch(int* rc) {
+  int dev = 0;
+  *rc = hip_status(hipGetDevice(&dev));
+  if (*rc) return nullptr;
+  if (dev < 0 || dev >= kMaxDevices) {
+    *rc = SWIFTSPEC_UNSUPPORTED;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    *rc = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (*rc) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
 }
 
 struct LayerWs {
@@ -404,6 +435,25 @@ int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, 
   run_attention(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_parent, T, Hq, Hkv, D,
                 rope_cos_sin, softmax_scale, out, ldo, nullptr, ws,
                 reinterpret_cast<float*>(static_cast<char*>(ws) + kHeader), S(stream));
+  return check_launch();
+}
+
+int swiftspec_tree_attention_noalloc(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
+                                     int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
+                                     const int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,
+                                     int32_t Hq, int32_t Hkv, int32_t D, const float* rope_cos_sin,
+                                     float softmax_scale, uint16_t* out, int32_t ldo, uint32_t* d_error,
+                                     void* stream) {
+  int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len,
+                                     d_parent, T, Hq, Hkv, D, rope_cos_sin, out, ldo);
+  if (rc) return rc;
+  if (ss::plan_tree_attention(T, Hq, Hkv, D, S_max).part_bytes > SWIFTSPEC_NOALLOC_SCRATCH_BYTES)
+    return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  float* part = static_cast<float*>(noalloc_scratch(&rc));
+  if (rc) return rc;
+  // the kernels OR device errors into word 0 of `ws`: here the caller's word
+  run_attention(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_parent, T, Hq, Hkv, D,
+                rope_cos_sin, softmax_scale, out, ldo, nullptr, d_error, part, S(stream));
   return check_launch();
 }
 

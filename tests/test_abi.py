@@ -107,6 +107,15 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert reorg(8, D=100) == ss.UNSUPPORTED
     assert reorg(8, stride=100) == ss.INVALID_ARG
     assert reorg(8, last=None) == ss.INVALID_ARG
+    # allocation-free attention: partials beyond the library's scratch array
+    # (1024 KV heads of 64 tokens: 2048 partials of 16.6 KB) are refused
+    na = lambda Hq, Hkv, T=64: lib.swiftspec_tree_attention_noalloc(fake, Hq * 128, fake, fake, Hkv * 128, fake,
+                                                                    fake, 4096 + T, fake, fake, T, Hq, Hkv, 128,
+                                                                    fake, 0.088, fake, Hq * 128, None, None)
+    assert na(1024, 1024) == ss.WORKSPACE_TOO_SMALL
+    assert na(64, 8, T=65) == ss.UNSUPPORTED
+    assert lib.swiftspec_tree_attention_noalloc(None, 8192, fake, fake, 1024, fake, fake, 4128, fake, fake, 32,
+                                                64, 8, 128, fake, 0.088, fake, 8192, None, None) == ss.INVALID_ARG
     # the renumbered forest may not be written over the forest being read
     alias = lambda par, newp: lib.swiftspec_kv_reorganize(fake, fake, 2, 8 * 200 * 128, 8, 200, 128, fake, par, 8,
                                                           fake, fake, newp, None, 0, None, 0, None)

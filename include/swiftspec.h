@@ -199,12 +199,12 @@ int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, 
  * (device uint32, nullable) receives the device error bits
  * (SWIFTSPEC_DEVERR_*, OR-ed in; the caller clears it).  A shape whose
  * partials do not fit returns SWIFTSPEC_WORKSPACE_TOO_SMALL before any
- * launch (the Llama-3 1B/8B/70B shapes at T <= 64 need at most 8.5 MB).
+ * launch (the Llama-3 1B/8B/70B shapes at T <= 64 need at most 17.2 MB).
  * The first call on a device looks up the array's device address
  * (SWIFTSPEC_HIP_ERROR if that fails).  No call allocates or frees memory.
  * Every call on one GPU shares its array: calls that overlap in time on one
  * GPU (several streams or threads) race, and their results are undefined. */
-#define SWIFTSPEC_NOALLOC_SCRATCH_BYTES (16u << 20)
+#define SWIFTSPEC_NOALLOC_SCRATCH_BYTES (32u << 20)
 int swiftspec_tree_attention_noalloc(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,
                                      int32_t ldkv, uint16_t* k_cache, uint16_t* v_cache, int32_t S_max,
                                      const int32_t* d_prefix_len, const int32_t* d_parent, int32_t T,

@@ -307,7 +307,7 @@ def tree_attention(q, k, v, k_cache, v_cache, prefix_len, parent, Hq, Hkv, D, ro
     _check(st, "tree_attention")
 
 
-NOALLOC_SCRATCH_BYTES = 16 << 20
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 def tree_attention_noalloc(q, k, v, k_cache, v_cache, prefix_len, parent, Hq, Hkv, D, rope, out, error=None,

@@ -47,12 +47,11 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
 // not a valid increasing tree; then anc = own bit and depth = 0.
 // kForest: any node may be a root (parent -1), as in a draft model's tree
 // cache below its last prefix token; otherwise node 0 is the only root.
+// tree_masks_from: the same from the parent value p of node `lane` (-1 for
+// lanes >= T), already loaded by the caller.
 template <bool kForest = false>
-__device__ __forceinline__ bool tree_masks_wave(const int32_t* __restrict__ parent, int T,
-                                                uint64_t& anc, int& depth) {
+__device__ __forceinline__ bool tree_masks_from(int p, int T, uint64_t& anc, int& depth) {
   const int lane = lane_id();
-  int p = -1;
-  if (lane < T) p = parent[lane];
   bool ok = lane >= T || (kForest ? (p >= -1 && p < lane) : (lane == 0 ? p == -1 : (p >= 0 && p < lane)));
   const bool all_ok = __all(ok);
   uint64_t a = lane < T ? (1ull << lane) : 0ull;
@@ -75,6 +74,12 @@ __device__ __forceinline__ bool tree_masks_wave(const int32_t* __restrict__ pare
   anc = a;
   depth = __popcll(a) - 1;
   return true;
+}
+template <bool kForest = false>
+__device__ __forceinline__ bool tree_masks_wave(const int32_t* __restrict__ parent, int T,
+                                                uint64_t& anc, int& depth) {
+  const int lane = lane_id();
+  return tree_masks_from<kForest>(lane < T ? parent[lane] : -1, T, anc, depth);
 }
 
 // fp16 bit helpers

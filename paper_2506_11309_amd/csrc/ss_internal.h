@@ -81,7 +81,8 @@ struct AttnPlan {
   int nsplit, chunk;
   size_t part_bytes;
 };
-AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max);
+// draft: the draft model's kernel (non-square mask); else the target kernel
+AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max, bool draft);
 void launch_tree_attention(const AttnLaunch& L, hipStream_t st);
 
 void launch_rmsnorm(const uint16_t* x, int M, int H, int ldx, const uint16_t* gamma, float eps,

@@ -119,9 +119,15 @@ int check_tree_attention_args(const uint16_t* q, int ldq, const uint16_t* k, con
   return SWIFTSPEC_OK;
 }
 
+// partial bytes of the target or the draft attention kernel, whichever is larger
+size_t attn_part_bytes(int T, int Hq, int Hkv, int D, int S_max) {
+  const size_t a = ss::plan_tree_attention(T, Hq, Hkv, D, S_max, false).part_bytes;
+  const size_t b = ss::plan_tree_attention(T, Hq, Hkv, D, S_max, true).part_bytes;
+  return a > b ? a : b;
+}
+
 size_t attn_ws(int T, int Hq, int Hkv, int D, int S_max) {
-  ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max);
-  return kHeader + align_up(p.part_bytes);
+  return kHeader + align_up(attn_part_bytes(T, Hq, Hkv, D, S_max));
 }
 
 void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v, int ldkv,
@@ -129,7 +135,7 @@ void run_attention(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t
                    int T, int Hq, int Hkv, int D, const float* rope, float scale, uint16_t* out,
                    int ldo, uint16_t* out_prep, void* ws, float* part, hipStream_t st, int N = 0,
                    const int32_t* cache_parent = nullptr, const int32_t* leaf_parent = nullptr) {
-  ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max);
+  ss::AttnPlan p = ss::plan_tree_attention(T, Hq, Hkv, D, S_max, N > 0 || leaf_parent != nullptr);
   ss::AttnLaunch L;
   L.N = N;
   L.cache_parent = cache_parent;
@@ -220,7 +226,7 @@ LayerWs layer_ws(const swiftspec_dims* d, int T) {
   upd(ss::plan_w4a16_gemm(T, d->Hq * d->D, d->H, false).part_bytes);
   upd(ss::plan_w4a16_gemm(T, d->H, d->F, true).part_bytes);
   upd(ss::plan_w4a16_gemm(T, d->F, d->H, false).part_bytes);
-  upd(ss::plan_tree_attention(T, d->Hq, d->Hkv, d->D, d->S_max).part_bytes);
+  upd(attn_part_bytes(T, d->Hq, d->Hkv, d->D, d->S_max));
   w.part = take(part);
   w.total = off;
   return w;
@@ -447,7 +453,7 @@ int swiftspec_tree_attention_noalloc(const uint16_t* q, int32_t ldq, const uint1
   int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len,
                                      d_parent, T, Hq, Hkv, D, rope_cos_sin, out, ldo);
   if (rc) return rc;
-  if (ss::plan_tree_attention(T, Hq, Hkv, D, S_max).part_bytes > SWIFTSPEC_NOALLOC_SCRATCH_BYTES)
+  if (ss::plan_tree_attention(T, Hq, Hkv, D, S_max, false).part_bytes > SWIFTSPEC_NOALLOC_SCRATCH_BYTES)
     return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   float* part = static_cast<float*>(noalloc_scratch(&rc));
   if (rc) return rc;

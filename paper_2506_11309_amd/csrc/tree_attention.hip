@@ -27,6 +27,8 @@
 // stream merges the S + 1 partials of a row block in split order, so
 // results are deterministic.  blockIdx % Hkv = g keeps one head's
 // workgroups on one XCD when Hkv divides 8.
+#include <type_traits>
+
 #include "ss_device.h"
 #include "ss_internal.h"
 
@@ -90,7 +92,7 @@ template <int D>
 __host__ __device__ constexpr size_t attn_part_bytes(int waves) {
   return (size_t)waves * (D / 16) * kWave * 8 + (size_t)waves * 16 * 4;
 }
-constexpr int kMaxParts = 16;  // prefix splits + tree split, merged in one pass
+constexpr int kMaxParts = 32;  // prefix splits + tree split, merged in one pass
 
 template <int D, int W>
 __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
@@ -451,48 +453,65 @@ __global__ __launch_bounds__(64 * W) void tree_attention_kernel(AttnArgs a) {
   if (kq == 0) lse[wave * 16 + n16] = l_run > 0.f ? m_run + __log2f(l_run) : -INFINITY;
 }
 
-// Merge of the S + 1 <= 16 partials of one 16-row x 16-column output tile,
+// Merge of the S + 1 <= NP partials of one 16-row x 16-column output tile,
 // in split order: with L_s the log-sum-exp of a row in split s and O_s its
 // normalised output, O = sum_s 2^(L_s - L) O_s, L = log2 sum_s 2^L_s (taken
 // relative to max_s L_s).  One wave per tile (lane: rows 4 (lane / 16) + r,
 // column lane % 16); every split's loads are issued at once, so the kernel
-// is one memory round trip long.  Grid = Hkv x RB x W x D/16.  A row that no
-// split saw (only when the attention kernel rejected the tree or the prefix
-// and published empty partials) is not written.
-template <int D, int W>
+// is one memory round trip long.  Grid = Hkv x RB x W x D/16 with the KV
+// head in blockIdx % Hkv, so that with 8 KV heads a head's merge runs on the
+// XCD whose L2 holds the head's partials (round-robin dispatch puts
+// blockIdx % 8 on XCD blockIdx % 8, as for the attention kernel).  A row that
+// no split saw (only when the attention kernel rejected the tree or the
+// prefix and published empty partials) is not written.
+template <int D, int W, int NP>
 __global__ __launch_bounds__(64) void tree_attention_merge_kernel(AttnArgs a) {
   constexpr int DT = D / 16;
   const int lane = lane_id();
   const int n16 = lane & 15, kq = lane >> 4;
-  const int dt = blockIdx.x % DT;
-  const int wave = (blockIdx.x / DT) % W;
-  const int grp = blockIdx.x / (DT * W);  // g * RB + rb
-  const int g = grp / a.RB, rb = grp % a.RB;
+  const int g = blockIdx.x % a.Hkv;
+  const int rest = blockIdx.x / a.Hkv;
+  const int dt = rest % DT;
+  const int wave = (rest / DT) % W;
+  const int rb = rest / (DT * W);
+  const int grp = g * a.RB + rb;
   const int nparts = a.nsplit + 1;
   const size_t part_stride = attn_part_bytes<D>(W);
   const char* base = reinterpret_cast<const char*>(a.part) + (size_t)grp * nparts * part_stride;
-  f32x4 ls[kMaxParts];
-  u32x2 ov[kMaxParts];
+  // the group's partials as one buffer: part j at scalar offset j * stride
+  const auto rp = buffer_rsrc(base, (uint32_t)(nparts * part_stride));
+  const uint32_t off_l = (uint32_t)(W * DT * kWave * 8 + (wave * 16 + 4 * kq) * 4);
+  const uint32_t off_o = (uint32_t)(((wave * DT + dt) * kWave + lane) * 8);
+  f32x4 ls[NP];
+  u32x2 ov[NP];
 #pragma unroll
-  for (int j = 0; j < kMaxParts; ++j) {
-    const char* src = base + (size_t)(j < nparts ? j : nparts - 1) * part_stride;
-    ls[j] = *reinterpret_cast<const f32x4*>(src + (size_t)W * DT * kWave * 8 + (wave * 16 + 4 * kq) * 4);
-    ov[j] = *reinterpret_cast<const u32x2*>(src + ((size_t)(wave * DT + dt) * kWave + lane) * 8);
+  for (int j = 0; j < NP; ++j) {
+    const uint32_t soff = (uint32_t)((j < nparts ? j : nparts - 1) * part_stride);
+    ls[j] = bitcast<f32x4>(buffer_load_x4(rp, off_l, soff));
+    ov[j] = bitcast<u32x2>(__builtin_amdgcn_raw_buffer_load_b64(rp, off_o, soff, 0));
   }
+  // branch-free: parts past nparts weigh 2^-inf = 0
+#pragma unroll
+  for (int j = 0; j < NP; ++j)
+    if (j >= nparts) ls[j] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
   float lmax[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
-  for (int j = 0; j < kMaxParts; ++j)
+  for (int j = 0; j < NP; ++j)
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (j < nparts) lmax[r] = fmaxf(lmax[r], ls[j][r]);
+    for (int r = 0; r < 4; ++r) lmax[r] = fmaxf(lmax[r], ls[j][r]);
+  // a row that no split saw keeps lmax = -inf: its weights are computed
+  // against 0 (all zero) and the row is not written
+  float ref[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) ref[r] = lmax[r] == -INFINITY ? 0.f : lmax[r];
   float wsum[4] = {0.f, 0.f, 0.f, 0.f}, acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int j = 0; j < kMaxParts; ++j)
+  for (int j = 0; j < NP; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float w = (j < nparts && ls[j][r] != -INFINITY) ? exp2f(ls[j][r] - lmax[r]) : 0.f;
+      const float w = __builtin_amdgcn_exp2f(ls[j][r] - ref[r]);
       wsum[r] += w;
-      acc[r] += w * h2f((uint16_t)(ov[j][r >> 1] >> (16 * (r & 1))));
+      acc[r] = __builtin_fmaf(w, h2f((uint16_t)(ov[j][r >> 1] >> (16 * (r & 1)))), acc[r]);
     }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
@@ -506,26 +525,501 @@ __global__ __launch_bounds__(64) void tree_attention_merge_kernel(AttnArgs a) {
   }
 }
 
+// merge launch: the partial count decides how many loads a lane issues
+template <int D, int W>
+static void launch_merge(const AttnArgs& a, hipStream_t st) {
+  const dim3 mgrid(a.Hkv * a.RB * W * (D / 16));
+  if (a.nsplit + 1 <= 16) hipLaunchKernelGGL((tree_attention_merge_kernel<D, W, 16>), mgrid, dim3(64), 0, st, a);
+  else hipLaunchKernelGGL((tree_attention_merge_kernel<D, W, kMaxParts>), mgrid, dim3(64), 0, st, a);
+}
+
+
+// ============================================================================
+// Target model (square tree mask, no tree cache).  The prefix keys stream
+// in 32-key stages fetched straight into LDS by 16-byte buffer loads to LDS
+// (lane i of a wave's load lands at 16-byte chunk i of a 1 KB block whose
+// base the wave chooses), up to 8 stages deep, so no register ring is needed
+// and up to seven stages (112 KB) are in flight per workgroup.  Every wave
+// keeps 32 query rows (two 16-row tiles sharing each K and V fragment read
+// from LDS); workgroups of 8 waves hold 256 rows, two waves per SIMD.
+// LDS layout of one stage (see KvLds): 1 KB blocks of key rows at a stride
+// of 1088 (K) or 1152 (V) bytes, and within a block row i the 16-byte chunk
+// c of the row stored at chunk c ^ x(i); each lane of a load fetches the
+// global chunk that belongs at its position.  With these the K-fragment
+// reads (16 rows, one chunk each) and the transposed V reads (8 rows, 32
+// bytes each) hit every bank once, and all K reads of a lane are one base
+// register plus immediate offsets.  Softmax: per-row reference maximum
+// raised lazily (only when a stage's maximum exceeds it by more than 2^8;
+// the unnormalised probabilities stay below 256, with fp16's relative
+// precision), row sums formed by the matrix cores (P times a ones column).
+// Partials use the merge kernel's layout with two 16-row "virtual waves" per
+// wave.
+constexpr int kFastKeys = 32;         // keys per LDS stage
+constexpr float kLazyRescale = 8.0f;  // log2 of the largest unnormalised probability
+
+template <int D>
+struct KvLds {
+  static constexpr int kCpr = D / 8;                // 16-byte chunks per key row
+  static constexpr int kRpb = 1024 / (2 * D);       // key rows per 1 KB block
+  static constexpr int kBlocks = kFastKeys / kRpb;  // blocks per matrix and stage
+  static constexpr int kKStride = 1088, kVStride = 1152;
+  static constexpr int kKBytes = kBlocks * kKStride;
+  static constexpr int kStage = kKBytes + kBlocks * kVStride;
+  // chunk XOR of row i of a block: K on chunk bits 0-1, V on bits 1-2
+  static __device__ __forceinline__ int xk(int i) { return D == 128 ? i : i >> 1; }
+  static __device__ __forceinline__ int xv(int i) { return D == 128 ? 2 * i : 2 * (i >> 1); }
+  // byte offsets of chunk c of stage key row `key` in the K / V region
+  static __device__ __forceinline__ int k_off(int key, int c) {
+    const int b = key / kRpb, i = key % kRpb;
+    return b * kKStride + i * 2 * D + ((c ^ xk(i)) << 4);
+  }
+  static __device__ __forceinline__ int v_off(int key, int c) {
+    const int b = key / kRpb, i = key % kRpb;
+    return kKBytes + b * kVStride + i * 2 * D + ((c ^ xv(i)) << 4);
+  }
+};
+
+// 16-byte buffer load of every lane straight into LDS: lane l's 16 bytes
+// (at voff + soff of the buffer) land at LDS address lds_addr + 16 l.  M0,
+// which holds the LDS base of such loads, is saved and restored around the
+// load (one wait state after setting it), so the compiler's own use of M0 is
+// untouched.  The compiler does not see the LDS write: the caller waits for
+// it with vmcnt and orders it against LDS reads with barriers.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 raw_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  return i32x4{(int)(uint32_t)b, (int)(uint32_t)(b >> 32), (int)bytes, 0x00020000};
+}
+__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %4\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, %3 offen lds\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(rsrc), "s"(soff), "s"(lds_addr)
+      : "memory");
+}
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding;
+// expcnt and lgkmcnt are left alone.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+// wait until at most `behind` stages (LPW loads each) of this wave remain in flight
+template <int LPW, int K>
+__device__ __forceinline__ void vm_wait_stages(int behind) {
+  if constexpr (K == 0) {
+    vm_wait<0>();
+  } else {
+    if (behind >= K) vm_wait<LPW * K>();
+    else vm_wait_stages<LPW, K - 1>(behind);
+  }
+}
+
+// Stages per workgroup: about 70 KB of LDS, so that two workgroups share a
+// compute unit (two waves per SIMD, from workgroups whose barriers are
+// independent, so one's matrix-core work overlaps the other's softmax).
+template <int D, int W>
+struct FastAttnCfg {
+  static constexpr int kLoadsPerWave = 2 * KvLds<D>::kBlocks / W;  // 1 KB loads per stage (K and V)
+  static constexpr int kStages = D == 128 ? 4 : 8;
+  static_assert(kLoadsPerWave * (kStages - 2) <= 63, "vmcnt range");
+  static_assert((2 * KvLds<D>::kBlocks) % W == 0, "stage split");
+};
+
+template <int D, int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ? 2 : 1))) void tree_attention_fast_kernel(AttnArgs a) {
+  using L = KvLds<D>;
+  using Cfg = FastAttnCfg<D, W>;
+  constexpr int NS = Cfg::kStages;
+  constexpr int LPW = Cfg::kLoadsPerWave;
+  constexpr int KS = D / 32;   // k-steps of the QK^T product
+  constexpr int DT = D / 16;   // d tiles of the PV product
+  constexpr int HALF = D / 2;
+  constexpr int VW = 2 * W;    // 16-row virtual waves of the partial layout
+  __shared__ __attribute__((aligned(16))) char kvs[NS * L::kStage];
+  __shared__ uint64_t s_anc[64];
+  __shared__ int32_t s_depth[64];
+  __shared__ int32_t s_status;
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n16 = lane & 15;
+  const int kq = lane >> 4;
+  const int g = blockIdx.x % a.Hkv;
+  const int rest = blockIdx.x / a.Hkv;
+  const int sp = rest % (a.nsplit + 1);
+  const int rb = rest / (a.nsplit + 1);
+  const bool tree_split = sp == a.nsplit;
+
+  // ---- prologue, two memory round trips: (1) this wave's raw query rows,
+  // the parent array (wave 0) and the prefix length; (2) after the tree
+  // masks, the rotary table rows at P + depth, while the first stages of
+  // keys and values (issued as soon as P is known) land ----
+  int node[2], qhead[2];
+  bool row_ok[2];
+  u32x4 qraw[2][KS];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int row = rb * (32 * W) + wave * 32 + t2 * 16 + n16;
+    row_ok[t2] = row < a.R;
+    node[t2] = row_ok[t2] ? row / a.G : 0;
+    qhead[t2] = g * a.G + (row_ok[t2] ? row % a.G : 0);
+    const uint16_t* qsrc = a.q + (size_t)node[t2] * a.ldq + qhead[t2] * D;
+#pragma unroll
+    for (int j = 0; j < KS; ++j)
+      qraw[t2][j] = row_ok[t2] ? *reinterpret_cast<const u32x4*>(qsrc + 32 * j + 8 * kq) : u32x4{0, 0, 0, 0};
+  }
+  const int par = (wave == 0 && lane < a.T) ? a.parent[lane] : -1;
+  const int P_dev = __builtin_amdgcn_readfirstlane(*a.prefix_len);
+  const bool p_ok = P_dev >= 0 && P_dev <= a.S_max - a.T;
+  const int P = p_ok ? P_dev : 0;
+  // this split's key range: stages [t0, t1) of the prefix's 32-key stages
+  int k_lo = 0, k_hi = 0, ntiles = 0;
+  if (!tree_split) {
+    const int tiles = (P + kFastKeys - 1) / kFastKeys;
+    const int t0 = sp * tiles / a.nsplit, t1 = (sp + 1) * tiles / a.nsplit;
+    k_lo = t0 * kFastKeys;
+    k_hi = min(P, t1 * kFastKeys);
+    ntiles = t1 - t0;
+  }
+  k_lo = __builtin_amdgcn_readfirstlane(k_lo);
+  k_hi = __builtin_amdgcn_readfirstlane(k_hi);
+  ntiles = __builtin_amdgcn_readfirstlane(ntiles);
+
+  // ---- tree masks and validity (wave 0) ----
+  if (wave == 0) {
+    uint64_t anc;
+    int depth;
+    const bool ok = tree_masks_from(par, a.T, anc, depth);
+    s_anc[lane] = anc;
+    s_depth[lane] = depth;
+    if (lane == 0) {
+      int st = 0;
+      if (!ok) st |= SWIFTSPEC_DEVERR_BAD_TREE;
+      if (!p_ok) st |= SWIFTSPEC_DEVERR_BAD_PREFIX;
+      s_status = st;
+      if (st && blockIdx.x == 0) report_error(a.ws, (uint32_t)st);
+    }
+  }
+
+  // ---- the first stages of keys and values ----
+  // the head's cache rows as buffer resources (loads past the last row
+  // return zeros; such keys are masked)
+  const uint32_t head_bytes = (uint32_t)((size_t)a.S_max * D * 2);
+  const i32x4 rk = raw_rsrc(a.k_cache + (size_t)g * a.S_max * D, head_bytes);
+  const i32x4 rv = raw_rsrc(a.v_cache + (size_t)g * a.S_max * D, head_bytes);
+  // this lane's part of every 1 KB block: row i of the block, the global
+  // chunk that belongs at its position (pos ^ x(i))
+  const int li = lane / L::kCpr, lpos = lane % L::kCpr;
+  const uint32_t voff_k = (uint32_t)(li * 2 * D + ((lpos ^ L::xk(li)) << 4));
+  const uint32_t voff_v = (uint32_t)(li * 2 * D + ((lpos ^ L::xv(li)) << 4));
+  // stage t (< ntiles) into slot t % NS: wave w issues block loads w, w + W,
+  // ... of the stage's K blocks followed by its V blocks (blocks wholly past
+  // k_hi reload the block holding row k_hi - 1)
+  const int last_blk_row = k_hi > 0 ? ((k_hi - 1) / L::kRpb) * L::kRpb : 0;
+  auto issue_tile = [&](int t) __attribute__((always_inline)) {
+    const int row0 = k_lo + t * kFastKeys;
+    const char* st = kvs + (t % NS) * L::kStage;
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      const int inst = i * W + wave;
+      const bool isv = inst >= L::kBlocks;
+      const int blk = isv ? inst - L::kBlocks : inst;
+      const uint32_t soff = (uint32_t)min(row0 + blk * L::kRpb, last_blk_row) * (uint32_t)(2 * D);
+      const char* dst = st + (isv ? L::kKBytes + blk * L::kVStride : blk * L::kKStride);
+      buffer_load_lds16(isv ? rv : rk, isv ? voff_v : voff_k, soff,
+                        __builtin_amdgcn_readfirstlane(lds_address(dst)));
+    }
+  };
+  if (p_ok) {
+#pragma unroll
+    for (int j = 0; j < NS - 1; ++j)
+      if (j < ntiles) issue_tile(j);
+  }
+  __syncthreads();
+  const int nparts = a.nsplit + 1;
+  const size_t grp = (size_t)g * a.RB + rb;
+  char* mine = reinterpret_cast<char*>(a.part) + (grp * nparts + sp) * attn_part_bytes<D>(VW);
+  float* lse = reinterpret_cast<float*>(mine + (size_t)VW * DT * kWave * 8);
+  if (s_status) {
+    // invalid tree or prefix: empty partials, so the merge leaves the output
+    // alone; the stage loads in flight land before the wave ends
+    if (tid < 16 * VW) lse[tid] = -INFINITY;
+    vm_wait<0>();
+    return;
+  }
+
+  // ---- this wave's 32 query rows (tiles t2 = 0, 1): rotated Q as B fragments ----
+  half8 qf[2][KS];
+  uint64_t anc[2];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    anc[t2] = s_anc[node[t2]];
+    float qv[KS][8];
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const half8 h = bitcast<half8>(qraw[t2][j]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qv[j][e] = (float)h[e];
+    }
+    const float* cs = a.rope + (size_t)(P + s_depth[node[t2]]) * D;  // [D/2][2]
+#pragma unroll
+    for (int j = 0; j < KS / 2; ++j) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int d = 32 * j + 8 * kq + e;  // < D/2; partner d + D/2 sits in k-step j + KS/2
+        const float c = cs[2 * d], sn = cs[2 * d + 1];
+        const float x1 = qv[j][e], x2 = qv[j + KS / 2][e];
+        qv[j][e] = x1 * c - x2 * sn;
+        qv[j + KS / 2][e] = x2 * c + x1 * sn;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      half8 h;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[e] = (_Float16)qv[j][e];
+      qf[t2][j] = h;
+    }
+  }
+
+  // per-row reference maximum (base 2, score layout: row n16 of tile t2),
+  // output and row-sum accumulators (O layout: rows 4 kq + r, column n16)
+  float m_ref[2] = {-INFINITY, -INFINITY};
+  f32x4 o[2][DT], ol[2];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    ol[t2] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[t2][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const half8 ones = {(_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f,
+                      (_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f};
+  const float c2 = a.scale_log2;
+  // LDS read offsets of this lane: K chunk 4 j + kq of key n16 (+ 16 h rows
+  // = 16 h / kRpb blocks, + 64 j bytes); V 8-byte piece (n16 % 4) of columns
+  // 16 dt + 4 (n16 % 4) of key 4 kq + n16 / 4 (+ 16 h rows), for dt % 4
+  // (D = 128: + 128 bytes for dt >= 4)
+  const int k_base = L::k_off(n16, kq);
+  int v_base[DT < 4 ? DT : 4];
+#pragma unroll
+  for (int d2 = 0; d2 < (DT < 4 ? DT : 4); ++d2)
+    v_base[d2] = L::v_off(4 * kq + (n16 >> 2), 2 * d2 + ((n16 & 3) >> 1)) + 8 * (n16 & 1);
+
+  // ---- one 32-key stage at sb: keys [0, key_end) valid (kMask), tree
+  // stages (kTree) also apply the ancestor-or-self mask of keys tree0 + k ----
+  auto compute = [&](const char* sb, int key_end, int tree0, auto mask_tag, auto tree_tag)
+      __attribute__((always_inline)) {
+    constexpr bool kMask = decltype(mask_tag)::value;
+    constexpr bool kTree = decltype(tree_tag)::value;
+    // S^T: lane holds keys 16 h + 4 kq + r (h < 2, r < 4) of query row n16
+    f32x4 s[2][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      half8 kf[KS];
+#pragma unroll
+      for (int j = 0; j < KS; ++j)
+        kf[j] = *reinterpret_cast<const half8*>(sb + k_base + (16 * h / L::kRpb) * L::kKStride + 64 * j);
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < KS; ++j) c = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[j], qf[t2][j], c, 0, 0, 0);
+        s[t2][h] = c;
+      }
+    }
+    float tmax[2];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      float mx = -INFINITY;
+      if constexpr (!kMask) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          mx = fmaxf(mx, fmaxf(fmaxf(s[t2][h][0], s[t2][h][1]), fmaxf(s[t2][h][2], s[t2][h][3])));
+      } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int kr = 16 * h + 4 * kq + r;
+            bool ok = kr < key_end;
+            if (kTree) ok = ok && ((anc[t2] >> (tree0 + kr)) & 1ull);
+            const float v = ok ? s[t2][h][r] : -INFINITY;
+            s[t2][h][r] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
+      tmax[t2] = quarter_reduce(mx, [](float x, float y) { return fmaxf(x, y); }) * c2;
+    }
+    // raise the reference maximum only when a row's maximum exceeds it by
+    // more than 2^8 (or the row saw its first key)
+    if (__any(tmax[0] > m_ref[0] + kLazyRescale || tmax[1] > m_ref[1] + kLazyRescale)) {
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        const float mn = fmaxf(m_ref[t2], tmax[t2]);
+        const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_ref[t2] - mn);
+        m_ref[t2] = mn;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float ar = __shfl(alpha, 4 * kq + r, kWave);
+          ol[t2][r] *= ar;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[t2][dt][r] *= ar;
+        }
+      }
+    }
+    // probabilities 2^(c s - m) <= 2^8 as the fp16 A fragment: slot
+    // 8 kq + 4 h + r holds key 16 h + 4 kq + r
+    half8 pf[2];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const float mu = m_ref[t2] == -INFINITY ? 0.f : m_ref[t2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          pf[t2][h * 4 + r] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[t2][h][r], c2, -mu));
+      ol[t2] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[t2], ones, ol[t2], 0, 0, 0);  // row sums
+    }
+    // O += P . V: V fragments by transposed reads, this lane addressing
+    // key 16 h + 4 kq + n16 / 4, columns 16 dt + 4 (n16 % 4) + 0..3
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      v4i16 hv[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const char* pv = sb + v_base[dt & 3] + (16 * h / L::kRpb) * L::kVStride + (dt >> 2) * 128;
+        hv[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(pv));
+      }
+      const half8 vf = bitcast<half8>(u32x4{bitcast<u32x2>(hv[0])[0], bitcast<u32x2>(hv[0])[1],
+                                            bitcast<u32x2>(hv[1])[0], bitcast<u32x2>(hv[1])[1]});
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) o[t2][dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[t2], vf, o[t2][dt], 0, 0, 0);
+    }
+  };
+
+  if (tree_split) {
+    // tree keys: rotate k at position P + depth, round to fp16; copy v; write
+    // both to the cache (row block 0) and to stages 0 and 1 (keys 0-31 and
+    // 32-63) in the stage layout
+    constexpr int kPairVecs = HALF / 8;
+    for (int idx = tid; idx < 64 * kPairVecs; idx += 64 * W) {
+      const int kr = idx / kPairVecs, c8 = (idx % kPairVecs) * 8;
+      u32x4 k1 = {0, 0, 0, 0}, k2 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0}, v2 = {0, 0, 0, 0};
+      if (kr < a.T) {
+        const uint16_t* ksrc = a.k + (size_t)kr * a.ldkv + g * D;
+        const uint16_t* vsrc = a.v + (size_t)kr * a.ldkv + g * D;
+        const u32x4 r1 = *reinterpret_cast<const u32x4*>(ksrc + c8);
+        const u32x4 r2 = *reinterpret_cast<const u32x4*>(ksrc + c8 + HALF);
+        v1 = *reinterpret_cast<const u32x4*>(vsrc + c8);
+        v2 = *reinterpret_cast<const u32x4*>(vsrc + c8 + HALF);
+        const float* cs = a.rope + (size_t)(P + s_depth[kr]) * D;
+        const half8 h1 = bitcast<half8>(r1), h2 = bitcast<half8>(r2);
+        half8 o1, o2;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float c = cs[2 * (c8 + e)], sn = cs[2 * (c8 + e) + 1];
+          const float x1 = (float)h1[e], x2 = (float)h2[e];
+          o1[e] = (_Float16)(x1 * c - x2 * sn);
+          o2[e] = (_Float16)(x2 * c + x1 * sn);
+        }
+        k1 = bitcast<u32x4>(o1);
+        k2 = bitcast<u32x4>(o2);
+        if (rb == 0) {
+          uint16_t* kd = a.k_cache + ((size_t)g * a.S_max + P + kr) * D;
+          uint16_t* vd = a.v_cache + ((size_t)g * a.S_max + P + kr) * D;
+          *reinterpret_cast<u32x4*>(kd + c8) = k1;
+          *reinterpret_cast<u32x4*>(kd + c8 + HALF) = k2;
+          *reinterpret_cast<u32x4*>(vd + c8) = v1;
+          *reinterpret_cast<u32x4*>(vd + c8 + HALF) = v2;
+        }
+      }
+      char* sb = kvs + (kr / kFastKeys) * L::kStage;
+      const int key = kr % kFastKeys, ca = c8 / 8, cb = (c8 + HALF) / 8;
+      *reinterpret_cast<u32x4*>(sb + L::k_off(key, ca)) = k1;
+      *reinterpret_cast<u32x4*>(sb + L::k_off(key, cb)) = k2;
+      *reinterpret_cast<u32x4*>(sb + L::v_off(key, ca)) = v1;
+      *reinterpret_cast<u32x4*>(sb + L::v_off(key, cb)) = v2;
+    }
+    __syncthreads();
+    compute(kvs, a.T, 0, std::true_type{}, std::true_type{});
+    if (a.T > kFastKeys) compute(kvs + L::kStage, a.T - kFastKeys, kFastKeys, std::true_type{}, std::true_type{});
+  } else {
+    // step t: wait for stage t (this wave's loads; later stages may stay in
+    // flight), barrier (every wave's loads of stage t have landed and every
+    // wave is done with stage t - 1), refill stage t - 1's slot with stage
+    // t + NS - 1, compute stage t (the last one masked past k_hi)
+    // (every stage but the last is full: the loop has one unmasked body)
+    for (int t = 0; t < ntiles - 1; ++t) {
+      vm_wait_stages<LPW, NS - 2>(ntiles - 1 - t);
+      lds_barrier();
+      if (t + NS - 1 < ntiles) issue_tile(t + NS - 1);
+      compute(kvs + (t % NS) * L::kStage, kFastKeys, 0, std::false_type{}, std::false_type{});
+    }
+    if (ntiles > 0) {
+      const int t = ntiles - 1;
+      vm_wait<0>();
+      lds_barrier();
+      compute(kvs + (t % NS) * L::kStage, k_hi - (k_lo + t * kFastKeys), 0, std::true_type{}, std::false_type{});
+    }
+  }
+
+  // ---- publish this split's partial (merged by the next kernel) ----
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int vw = 2 * wave + t2;
+    float inv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) inv[r] = ol[t2][r] > 0.f ? 1.0f / ol[t2][r] : 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const uint32_t lo = (uint32_t)f2h(o[t2][dt][0] * inv[0]) | ((uint32_t)f2h(o[t2][dt][1] * inv[1]) << 16);
+      const uint32_t hi = (uint32_t)f2h(o[t2][dt][2] * inv[2]) | ((uint32_t)f2h(o[t2][dt][3] * inv[3]) << 16);
+      *reinterpret_cast<u32x2*>(mine + ((size_t)(vw * DT + dt) * kWave + lane) * 8) = u32x2{lo, hi};
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float mr = __shfl(m_ref[t2], 4 * kq + r, kWave);
+      if (n16 == 0) lse[vw * 16 + 4 * kq + r] = ol[t2][r] > 0.f ? mr + __log2f(ol[t2][r]) : -INFINITY;
+    }
+  }
+}
+
+// query rows per workgroup of the target kernel: 32 per wave, up to 4 waves
+static int fast_attn_waves(int R) { return R <= 32 ? 1 : R <= 64 ? 2 : 4; }
+
 static int attn_waves(int R) { return R >= 128 ? 8 : 4; }
 
-AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max) {
+AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max, bool draft) {
   AttnPlan p;
   const int G = Hq / Hkv;
   const int R = T * G;
-  const int W = attn_waves(R);
-  const int RB = (R + 16 * W - 1) / (16 * W);
+  // rows per workgroup: draft kernel 16 per wave (4 or 8 waves), target
+  // kernel 32 per wave (1, 2 or 4 waves); partials in 16-row virtual waves
+  const int VW = draft ? attn_waves(R) : 2 * fast_attn_waves(R);
+  const int RB = (R + 16 * VW - 1) / (16 * VW);
   const int groups = Hkv * RB;
   // about 256 workgroups in flight, at least two key tiles per prefix split
   // (four: no change at the 70B shapes, 2 us slower at prefixes of 500-1000
   // keys with few KV heads; one: slower at 1000 keys)
-  int ns = 256 / groups - 1;
+  // about two workgroups per compute unit for the target kernel (one for the
+  // draft kernel)
+  int ns = (draft ? 256 : 512) / groups - 1;
   const int max_tiles = (S_max - T + kKeyTile - 1) / kKeyTile;
   if (ns > max_tiles / 2) ns = max_tiles / 2;
-  if (ns > kMaxParts - 1) ns = kMaxParts - 1;
+  const int max_parts = draft ? 16 : kMaxParts;  // the draft kernel keeps its 16-part plan
+  if (ns > max_parts - 1) ns = max_parts - 1;
   if (ns < 1) ns = 1;
   p.nsplit = ns;
   p.chunk = 0;
-  const size_t part_stride = D == 64 ? attn_part_bytes<64>(W) : attn_part_bytes<128>(W);
+  const size_t part_stride = D == 64 ? attn_part_bytes<64>(VW) : attn_part_bytes<128>(VW);
   p.part_bytes = (size_t)groups * (ns + 1) * part_stride;
   return p;
 }
@@ -556,27 +1050,44 @@ void launch_tree_attention(const AttnLaunch& L, hipStream_t st) {
   a.Hkv = L.Hkv;
   a.G = L.Hq / L.Hkv;
   a.R = L.T * a.G;
-  const int W = attn_waves(a.R);
-  a.RB = (a.R + 16 * W - 1) / (16 * W);
   a.nsplit = L.nsplit;
   a.scale_log2 = L.scale * 1.4426950408889634f;
+  const bool draft = L.N > 0 || L.leaf_parent != nullptr;
+  if (!draft) {
+    // target model: direct-to-LDS kernel, 32 rows per wave, partials in
+    // 16-row virtual waves (2 per wave) for the merge kernel
+    const int W = fast_attn_waves(a.R);
+    a.RB = (a.R + 32 * W - 1) / (32 * W);
+    const dim3 grid(L.Hkv * a.RB * (L.nsplit + 1));
+#define SS_FAST(DD, WW)                                                                          \
+    hipLaunchKernelGGL((tree_attention_fast_kernel<DD, WW>), grid, dim3(64 * WW), 0, st, a);     \
+    launch_merge<DD, 2 * WW>(a, st)
+    if (L.D == 64) {
+      if (W == 1) { SS_FAST(64, 1); } else if (W == 2) { SS_FAST(64, 2); } else { SS_FAST(64, 4); }
+    } else {
+      if (W == 1) { SS_FAST(128, 1); } else if (W == 2) { SS_FAST(128, 2); } else { SS_FAST(128, 4); }
+    }
+#undef SS_FAST
+    return;
+  }
+  const int W = attn_waves(a.R);
+  a.RB = (a.R + 16 * W - 1) / (16 * W);
   const dim3 grid(L.Hkv * a.RB * (L.nsplit + 1));
-  const dim3 mgrid(L.Hkv * a.RB * W * (L.D / 16));
   if (W == 8) {
     if (L.D == 64) {
       hipLaunchKernelGGL((tree_attention_kernel<64, 8>), grid, dim3(512), 0, st, a);
-      hipLaunchKernelGGL((tree_attention_merge_kernel<64, 8>), mgrid, dim3(64), 0, st, a);
+      launch_merge<64, 8>(a, st);
     } else {
       hipLaunchKernelGGL((tree_attention_kernel<128, 8>), grid, dim3(512), 0, st, a);
-      hipLaunchKernelGGL((tree_attention_merge_kernel<128, 8>), mgrid, dim3(64), 0, st, a);
+      launch_merge<128, 8>(a, st);
     }
   } else {
     if (L.D == 64) {
       hipLaunchKernelGGL((tree_attention_kernel<64, 4>), grid, dim3(256), 0, st, a);
-      hipLaunchKernelGGL((tree_attention_merge_kernel<64, 4>), mgrid, dim3(64), 0, st, a);
+      launch_merge<64, 4>(a, st);
     } else {
       hipLaunchKernelGGL((tree_attention_kernel<128, 4>), grid, dim3(256), 0, st, a);
-      hipLaunchKernelGGL((tree_attention_merge_kernel<128, 4>), mgrid, dim3(64), 0, st, a);
+      launch_merge<128, 4>(a, st);
     }
   }
 }

@@ -25,7 +25,7 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
 # accumulators in ordinary vector registers (the default accumulation-register
 # form makes the compiler copy the output tiles between the two register
 # files around every key tile)
-EXTRA = {"tree_attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+EXTRA = {"tree_attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"]}
 
 
 def _compile(src: str, verbose: bool) -> str:

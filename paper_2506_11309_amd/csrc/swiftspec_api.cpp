@@ -107,8 +107,9 @@ void run_gemm_plain(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16
 int check_tree_attention_args(const uint16_t* q, int ldq, const uint16_t* k, const uint16_t* v,
                               int ldkv, const uint16_t* kc, const uint16_t* vc, int S_max,
                               const int32_t* P, const int32_t* parent, int T, int Hq, int Hkv,
-                              int D, const float* rope, const uint16_t* out, int ldo) {
+                              int D, const float* rope, float scale, const uint16_t* out, int ldo) {
   if (!q || !k || !v || !kc || !vc || !P || !parent || !rope || !out) return SWIFTSPEC_INVALID_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SWIFTSPEC_INVALID_ARG;
   if (T < 1 || Hq < 1 || Hkv < 1 || S_max < T) return SWIFTSPEC_INVALID_ARG;
   if (T > SWIFTSPEC_MAX_TREE || (D != 64 && D != 128) || Hq % Hkv != 0) return SWIFTSPEC_UNSUPPORTED;
   if (ldq < Hq * D || ldkv < Hkv * D || ldo < Hq * D) return SWIFTSPEC_INVALID_ARG;
@@ -434,7 +435,7 @@ int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, 
                              float softmax_scale, uint16_t* out, int32_t ldo, void* ws,
                              size_t ws_bytes, void* stream) {
   int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len,
-                                     d_parent, T, Hq, Hkv, D, rope_cos_sin, out, ldo);
+                                     d_parent, T, Hq, Hkv, D, rope_cos_sin, softmax_scale, out, ldo);
   if (rc) return rc;
   if (!ws) return SWIFTSPEC_INVALID_ARG;
   if (ws_bytes < attn_ws(T, Hq, Hkv, D, S_max)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
@@ -451,7 +452,7 @@ int swiftspec_tree_attention_noalloc(const uint16_t* q, int32_t ldq, const uint1
                                      float softmax_scale, uint16_t* out, int32_t ldo, uint32_t* d_error,
                                      void* stream) {
   int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len,
-                                     d_parent, T, Hq, Hkv, D, rope_cos_sin, out, ldo);
+                                     d_parent, T, Hq, Hkv, D, rope_cos_sin, softmax_scale, out, ldo);
   if (rc) return rc;
   if (ss::plan_tree_attention(T, Hq, Hkv, D, S_max, false).part_bytes > SWIFTSPEC_NOALLOC_SCRATCH_BYTES)
     return SWIFTSPEC_WORKSPACE_TOO_SMALL;
@@ -527,7 +528,7 @@ int swiftspec_draft_tree_attention(const uint16_t* q, int32_t ldq, const uint16_
   // the same checks as the target attention over w new tokens (d_leaf_parent
   // stands in for the parent array)
   int rc = check_tree_attention_args(q, ldq, k, v, ldkv, k_cache, v_cache, S_max, d_prefix_len, d_leaf_parent, w,
-                                     Hq, Hkv, D, rope_cos_sin, out, ldo);
+                                     Hq, Hkv, D, rope_cos_sin, softmax_scale, out, ldo);
   if (rc) return rc;
   if (!ws) return SWIFTSPEC_INVALID_ARG;
   if (ws_bytes < attn_ws(w, Hq, Hkv, D, S_max)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;

@@ -541,7 +541,10 @@ static void launch_merge(const AttnArgs& a, hipStream_t st) {
 // base the wave chooses), up to 8 stages deep, so no register ring is needed
 // and up to seven stages (112 KB) are in flight per workgroup.  Every wave
 // keeps 32 query rows (two 16-row tiles sharing each K and V fragment read
-// from LDS); workgroups of 8 waves hold 256 rows, two waves per SIMD.
+// from LDS); workgroups of 1, 2 or 4 waves (two workgroups per compute unit)
+// or of 8 waves (one), two waves per SIMD either way.  The prologue makes
+// two memory round trips (parent array and queries; then the rotary rows at
+// P + depth, loaded ahead of the first stages).
 // LDS layout of one stage (see KvLds): 1 KB blocks of key rows at a stride
 // of 1088 (K) or 1152 (V) bytes, and within a block row i the 16-byte chunk
 // c of the row stored at chunk c ^ x(i); each lane of a load fetches the
@@ -551,7 +554,9 @@ static void launch_merge(const AttnArgs& a, hipStream_t st) {
 // register plus immediate offsets.  Softmax: per-row reference maximum
 // raised lazily (only when a stage's maximum exceeds it by more than 2^8;
 // the unnormalised probabilities stay below 256, with fp16's relative
-// precision), row sums formed by the matrix cores (P times a ones column).
+// precision), row sums formed by the matrix cores (P times a ones column);
+// a stage whose scores all stay within 2^8 of the reference takes no
+// cross-lane step (only a per-lane maximum and one wave-wide vote).
 // Partials use the merge kernel's layout with two 16-row "virtual waves" per
 // wave.
 constexpr int kFastKeys = 32;         // keys per LDS stage
@@ -610,6 +615,18 @@ __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
+// 16-byte global load issued as inline assembly: the compiler inserts no
+// wait for it (it does not see the load), so the caller waits with vm_wait
+// and then passes the value through after_wait, which the uses depend on
+__device__ __forceinline__ u32x4 load_x4_untracked(const void* p) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p));
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ void after_wait(T& x) {
+  asm volatile("" : "+v"(x));
+}
 // wait until at most `behind` stages (LPW loads each) of this wave remain in flight
 template <int LPW, int K>
 __device__ __forceinline__ void vm_wait_stages(int behind) {
@@ -628,7 +645,7 @@ template <int D, int W>
 struct FastAttnCfg {
   static constexpr int kLoadsPerWave = 2 * KvLds<D>::kBlocks / W;  // 1 KB loads per stage (K and V)
   static constexpr int kStages = D == 128 ? 4 : 8;
-  static_assert(kLoadsPerWave * (kStages - 2) <= 63, "vmcnt range");
+  static_assert(kLoadsPerWave * (kStages - 1) <= 63, "vmcnt range");
   static_assert((2 * KvLds<D>::kBlocks) % W == 0, "stage split");
 };
 
@@ -643,10 +660,6 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   constexpr int HALF = D / 2;
   constexpr int VW = 2 * W;    // 16-row virtual waves of the partial layout
   __shared__ __attribute__((aligned(16))) char kvs[NS * L::kStage];
-  __shared__ uint64_t s_anc[64];
-  __shared__ int32_t s_depth[64];
-  __shared__ int32_t s_status;
-
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -658,10 +671,11 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   const int rb = rest / (a.nsplit + 1);
   const bool tree_split = sp == a.nsplit;
 
-  // ---- prologue, two memory round trips: (1) this wave's raw query rows,
-  // the parent array (wave 0) and the prefix length; (2) after the tree
-  // masks, the rotary table rows at P + depth, while the first stages of
-  // keys and values (issued as soon as P is known) land ----
+  // ---- prologue, two memory round trips: (1) the parent array and this
+  // wave's raw query rows; (2) after the tree masks (every wave forms them
+  // for all nodes), the rotary rows at P + depth, issued ahead of the first
+  // key and value stages so that waiting for them leaves those in flight ----
+  const int par = lane < a.T ? a.parent[lane] : -1;
   int node[2], qhead[2];
   bool row_ok[2];
   u32x4 qraw[2][KS];
@@ -671,12 +685,10 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     row_ok[t2] = row < a.R;
     node[t2] = row_ok[t2] ? row / a.G : 0;
     qhead[t2] = g * a.G + (row_ok[t2] ? row % a.G : 0);
-    const uint16_t* qsrc = a.q + (size_t)node[t2] * a.ldq + qhead[t2] * D;
+    const uint16_t* qsrc = a.q + (size_t)node[t2] * a.ldq + qhead[t2] * D + 8 * kq;
 #pragma unroll
-    for (int j = 0; j < KS; ++j)
-      qraw[t2][j] = row_ok[t2] ? *reinterpret_cast<const u32x4*>(qsrc + 32 * j + 8 * kq) : u32x4{0, 0, 0, 0};
+    for (int j = 0; j < KS; ++j) qraw[t2][j] = load_x4_untracked(qsrc + 32 * j);
   }
-  const int par = (wave == 0 && lane < a.T) ? a.parent[lane] : -1;
   const int P_dev = __builtin_amdgcn_readfirstlane(*a.prefix_len);
   const bool p_ok = P_dev >= 0 && P_dev <= a.S_max - a.T;
   const int P = p_ok ? P_dev : 0;
@@ -693,20 +705,35 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   k_hi = __builtin_amdgcn_readfirstlane(k_hi);
   ntiles = __builtin_amdgcn_readfirstlane(ntiles);
 
-  // ---- tree masks and validity (wave 0) ----
-  if (wave == 0) {
-    uint64_t anc;
-    int depth;
-    const bool ok = tree_masks_from(par, a.T, anc, depth);
-    s_anc[lane] = anc;
-    s_depth[lane] = depth;
-    if (lane == 0) {
-      int st = 0;
-      if (!ok) st |= SWIFTSPEC_DEVERR_BAD_TREE;
-      if (!p_ok) st |= SWIFTSPEC_DEVERR_BAD_PREFIX;
-      s_status = st;
-      if (st && blockIdx.x == 0) report_error(a.ws, (uint32_t)st);
-    }
+  // ---- tree masks and validity ----
+  uint64_t anc_all;
+  int depth_all;
+  const bool tree_ok = tree_masks_from(par, a.T, anc_all, depth_all);
+  const int nparts = a.nsplit + 1;
+  const size_t grp = (size_t)g * a.RB + rb;
+  char* mine = reinterpret_cast<char*>(a.part) + (grp * nparts + sp) * attn_part_bytes<D>(VW);
+  float* lse = reinterpret_cast<float*>(mine + (size_t)VW * DT * kWave * 8);
+  if (!tree_ok || !p_ok) {
+    // invalid tree or prefix: empty partials, so the merge leaves the output
+    // alone (no key or value stage has been issued)
+    if (blockIdx.x == 0 && tid == 0)
+      report_error(a.ws, (tree_ok ? 0u : (uint32_t)SWIFTSPEC_DEVERR_BAD_TREE) |
+                             (p_ok ? 0u : (uint32_t)SWIFTSPEC_DEVERR_BAD_PREFIX));
+    if (tid < 16 * VW) lse[tid] = -INFINITY;
+    vm_wait<0>();
+    return;
+  }
+  uint64_t anc[2];
+  u32x4 csraw[2][KS / 2][4];  // cos/sin pairs of dimensions 32 j + 8 kq + 0..7
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    anc[t2] = shfl_u64(anc_all, node[t2]);
+    const int dep = __shfl(depth_all, node[t2], kWave);
+    const float* cs = a.rope + (size_t)(P + dep) * D;  // [D/2][2]
+#pragma unroll
+    for (int j = 0; j < KS / 2; ++j)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) csraw[t2][j][c] = load_x4_untracked(cs + 2 * (32 * j + 8 * kq) + 4 * c);
   }
 
   // ---- the first stages of keys and values ----
@@ -738,44 +765,38 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
                         __builtin_amdgcn_readfirstlane(lds_address(dst)));
     }
   };
-  if (p_ok) {
 #pragma unroll
-    for (int j = 0; j < NS - 1; ++j)
-      if (j < ntiles) issue_tile(j);
-  }
-  __syncthreads();
-  const int nparts = a.nsplit + 1;
-  const size_t grp = (size_t)g * a.RB + rb;
-  char* mine = reinterpret_cast<char*>(a.part) + (grp * nparts + sp) * attn_part_bytes<D>(VW);
-  float* lse = reinterpret_cast<float*>(mine + (size_t)VW * DT * kWave * 8);
-  if (s_status) {
-    // invalid tree or prefix: empty partials, so the merge leaves the output
-    // alone; the stage loads in flight land before the wave ends
-    if (tid < 16 * VW) lse[tid] = -INFINITY;
-    vm_wait<0>();
-    return;
-  }
+  for (int j = 0; j < NS - 1; ++j)
+    if (j < ntiles) issue_tile(j);
+  // the query and rotary loads, older than those stages, have landed
+  vm_wait_stages<LPW, NS - 1>(min(ntiles, NS - 1));
 
   // ---- this wave's 32 query rows (tiles t2 = 0, 1): rotated Q as B fragments ----
+  const float c2 = a.scale_log2;
   half8 qf[2][KS];
-  uint64_t anc[2];
 #pragma unroll
   for (int t2 = 0; t2 < 2; ++t2) {
-    anc[t2] = s_anc[node[t2]];
     float qv[KS][8];
 #pragma unroll
     for (int j = 0; j < KS; ++j) {
+      after_wait(qraw[t2][j]);
       const half8 h = bitcast<half8>(qraw[t2][j]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qv[j][e] = (float)h[e];
+      for (int e = 0; e < 8; ++e) qv[j][e] = row_ok[t2] ? (float)h[e] : 0.f;
     }
-    const float* cs = a.rope + (size_t)(P + s_depth[node[t2]]) * D;  // [D/2][2]
 #pragma unroll
     for (int j = 0; j < KS / 2; ++j) {
+      float cs[16];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        after_wait(csraw[t2][j][c]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[4 * c + e] = bitcast<float>(csraw[t2][j][c][e]);
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int d = 32 * j + 8 * kq + e;  // < D/2; partner d + D/2 sits in k-step j + KS/2
-        const float c = cs[2 * d], sn = cs[2 * d + 1];
+        // dimension 32 j + 8 kq + e (< D/2); its partner + D/2 sits in k-step j + KS/2
+        const float c = cs[2 * e], sn = cs[2 * e + 1];
         const float x1 = qv[j][e], x2 = qv[j + KS / 2][e];
         qv[j][e] = x1 * c - x2 * sn;
         qv[j + KS / 2][e] = x2 * c + x1 * sn;
@@ -790,9 +811,11 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     }
   }
 
-  // per-row reference maximum (base 2, score layout: row n16 of tile t2),
-  // output and row-sum accumulators (O layout: rows 4 kq + r, column n16)
-  float m_ref[2] = {-INFINITY, -INFINITY};
+  // per-row softmax state in the score layout (row n16 of tile t2), base 2:
+  // the reference exponent m_ref and the rescale threshold thr (m_ref +
+  // kLazyRescale once the row has seen a key, -inf before); output and row-sum
+  // accumulators (O layout: rows 4 kq + r, column n16)
+  float m_ref[2] = {0.f, 0.f}, thr[2] = {-INFINITY, -INFINITY};
   f32x4 o[2][DT], ol[2];
 #pragma unroll
   for (int t2 = 0; t2 < 2; ++t2) {
@@ -802,7 +825,6 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   }
   const half8 ones = {(_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f,
                       (_Float16)1.f, (_Float16)1.f, (_Float16)1.f, (_Float16)1.f};
-  const float c2 = a.scale_log2;
   // LDS read offsets of this lane: K chunk 4 j + kq of key n16 (+ 16 h rows
   // = 16 h / kRpb blocks, + 64 j bytes); V 8-byte piece (n16 % 4) of columns
   // 16 dt + 4 (n16 % 4) of key 4 kq + n16 / 4 (+ 16 h rows), for dt % 4
@@ -835,15 +857,11 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
         s[t2][h] = c;
       }
     }
-    float tmax[2];
+    // this lane's largest score of each tile (masked keys -inf)
+    float lm[2];
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
-      float mx = -INFINITY;
-      if constexpr (!kMask) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-          mx = fmaxf(mx, fmaxf(fmaxf(s[t2][h][0], s[t2][h][1]), fmaxf(s[t2][h][2], s[t2][h][3])));
-      } else {
+      if constexpr (kMask) {
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -851,21 +869,25 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
             const int kr = 16 * h + 4 * kq + r;
             bool ok = kr < key_end;
             if (kTree) ok = ok && ((anc[t2] >> (tree0 + kr)) & 1ull);
-            const float v = ok ? s[t2][h][r] : -INFINITY;
-            s[t2][h][r] = v;
-            mx = fmaxf(mx, v);
+            if (!ok) s[t2][h][r] = -INFINITY;
           }
       }
-      tmax[t2] = quarter_reduce(mx, [](float x, float y) { return fmaxf(x, y); }) * c2;
+      lm[t2] = fmaxf(fmaxf(fmaxf(s[t2][0][0], s[t2][0][1]), fmaxf(s[t2][0][2], s[t2][0][3])),
+                     fmaxf(fmaxf(s[t2][1][0], s[t2][1][1]), fmaxf(s[t2][1][2], s[t2][1][3])));
     }
-    // raise the reference maximum only when a row's maximum exceeds it by
-    // more than 2^8 (or the row saw its first key)
-    if (__any(tmax[0] > m_ref[0] + kLazyRescale || tmax[1] > m_ref[1] + kLazyRescale)) {
+    // move a row's reference up only when one of its scores exceeds it by
+    // more than 2^8 (the probabilities then stay below 256), and set it at
+    // the row's first key (scores scale by c2 > 0, so maxima commute with it)
+    if (__any(lm[0] * c2 > thr[0] || lm[1] * c2 > thr[1])) {
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2) {
-        const float mn = fmaxf(m_ref[t2], tmax[t2]);
-        const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_ref[t2] - mn);
+        const float rmax = quarter_reduce(lm[t2], [](float x, float y) { return fmaxf(x, y); }) * c2;
+        const bool seen = thr[t2] != -INFINITY;
+        const float mn = seen ? fmaxf(m_ref[t2], rmax) : (rmax == -INFINITY ? m_ref[t2] : rmax);
+        // rows that saw no key yet hold zero sums: their factor is 1
+        const float alpha = seen ? __builtin_amdgcn_exp2f(m_ref[t2] - mn) : 1.f;
         m_ref[t2] = mn;
+        if (seen || rmax != -INFINITY) thr[t2] = mn + kLazyRescale;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float ar = __shfl(alpha, 4 * kq + r, kWave);
@@ -875,17 +897,16 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
         }
       }
     }
-    // probabilities 2^(c s - m) <= 2^8 as the fp16 A fragment: slot
+    // probabilities 2^(c2 s - m_ref) <= 2^8 as the fp16 A fragment: slot
     // 8 kq + 4 h + r holds key 16 h + 4 kq + r
     half8 pf[2];
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
-      const float mu = m_ref[t2] == -INFINITY ? 0.f : m_ref[t2];
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          pf[t2][h * 4 + r] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[t2][h][r], c2, -mu));
+          pf[t2][h * 4 + r] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[t2][h][r], c2, -m_ref[t2]));
       ol[t2] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[t2], ones, ol[t2], 0, 0, 0);  // row sums
     }
     // O += P . V: V fragments by transposed reads, this lane addressing
@@ -912,6 +933,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     constexpr int kPairVecs = HALF / 8;
     for (int idx = tid; idx < 64 * kPairVecs; idx += 64 * W) {
       const int kr = idx / kPairVecs, c8 = (idx % kPairVecs) * 8;
+      const int kdep = __shfl(depth_all, kr, kWave);  // kr < 64; every lane takes part
       u32x4 k1 = {0, 0, 0, 0}, k2 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0}, v2 = {0, 0, 0, 0};
       if (kr < a.T) {
         const uint16_t* ksrc = a.k + (size_t)kr * a.ldkv + g * D;
@@ -920,7 +942,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
         const u32x4 r2 = *reinterpret_cast<const u32x4*>(ksrc + c8 + HALF);
         v1 = *reinterpret_cast<const u32x4*>(vsrc + c8);
         v2 = *reinterpret_cast<const u32x4*>(vsrc + c8 + HALF);
-        const float* cs = a.rope + (size_t)(P + s_depth[kr]) * D;
+        const float* cs = a.rope + (size_t)(P + kdep) * D;
         const half8 h1 = bitcast<half8>(r1), h2 = bitcast<half8>(r2);
         half8 o1, o2;
 #pragma unroll
@@ -992,8 +1014,13 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   }
 }
 
-// query rows per workgroup of the target kernel: 32 per wave, up to 4 waves
-static int fast_attn_waves(int R) { return R <= 32 ? 1 : R <= 64 ? 2 : 4; }
+// query rows per workgroup of the target kernel: 32 per wave, up to 4 waves,
+// or 8 (one workgroup per compute unit, each key and value stage landing once
+// for all 256 rows of a KV head) when a head has more than 128 rows and the
+// prefix may reach 16K keys, where streaming the cache dominates
+static int fast_attn_waves(int R, int P_max) {
+  return R <= 32 ? 1 : R <= 64 ? 2 : (R <= 128 || P_max < 16384) ? 4 : 8;
+}
 
 static int attn_waves(int R) { return R >= 128 ? 8 : 4; }
 
@@ -1003,18 +1030,21 @@ AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max, bool draf
   const int R = T * G;
   // rows per workgroup: draft kernel 16 per wave (4 or 8 waves), target
   // kernel 32 per wave (1, 2 or 4 waves); partials in 16-row virtual waves
-  const int VW = draft ? attn_waves(R) : 2 * fast_attn_waves(R);
+  const int VW = draft ? attn_waves(R) : 2 * fast_attn_waves(R, S_max - T);
   const int RB = (R + 16 * VW - 1) / (16 * VW);
   const int groups = Hkv * RB;
   // about 256 workgroups in flight, at least two key tiles per prefix split
   // (four: no change at the 70B shapes, 2 us slower at prefixes of 500-1000
   // keys with few KV heads; one: slower at 1000 keys)
-  // about two workgroups per compute unit for the target kernel (one for the
-  // draft kernel)
-  int ns = (draft ? 256 : 512) / groups - 1;
+  // about two workgroups per compute unit for the target kernel with up to 4
+  // waves (one for the 8-wave target workgroups and for the draft kernel)
+  int ns = (draft || VW == 16 ? 256 : 512) / groups - 1;
   const int max_tiles = (S_max - T + kKeyTile - 1) / kKeyTile;
   if (ns > max_tiles / 2) ns = max_tiles / 2;
-  const int max_parts = draft ? 16 : kMaxParts;  // the draft kernel keeps its 16-part plan
+  // at most 16 parts for the draft kernel, and for the target kernel when
+  // workgroups of up to 4 waves cover at least 8 row groups (there the merge,
+  // which re-reads every part, costs more than the longer splits)
+  const int max_parts = draft || (VW <= 8 && groups >= 8) ? 16 : kMaxParts;
   if (ns > max_parts - 1) ns = max_parts - 1;
   if (ns < 1) ns = 1;
   p.nsplit = ns;
@@ -1056,16 +1086,16 @@ void launch_tree_attention(const AttnLaunch& L, hipStream_t st) {
   if (!draft) {
     // target model: direct-to-LDS kernel, 32 rows per wave, partials in
     // 16-row virtual waves (2 per wave) for the merge kernel
-    const int W = fast_attn_waves(a.R);
+    const int W = fast_attn_waves(a.R, a.S_max - a.T);
     a.RB = (a.R + 32 * W - 1) / (32 * W);
     const dim3 grid(L.Hkv * a.RB * (L.nsplit + 1));
 #define SS_FAST(DD, WW)                                                                          \
     hipLaunchKernelGGL((tree_attention_fast_kernel<DD, WW>), grid, dim3(64 * WW), 0, st, a);     \
     launch_merge<DD, 2 * WW>(a, st)
     if (L.D == 64) {
-      if (W == 1) { SS_FAST(64, 1); } else if (W == 2) { SS_FAST(64, 2); } else { SS_FAST(64, 4); }
+      if (W == 1) { SS_FAST(64, 1); } else if (W == 2) { SS_FAST(64, 2); } else if (W == 4) { SS_FAST(64, 4); } else { SS_FAST(64, 8); }
     } else {
-      if (W == 1) { SS_FAST(128, 1); } else if (W == 2) { SS_FAST(128, 2); } else { SS_FAST(128, 4); }
+      if (W == 1) { SS_FAST(128, 1); } else if (W == 2) { SS_FAST(128, 2); } else if (W == 4) { SS_FAST(128, 4); } else { SS_FAST(128, 8); }
     }
 #undef SS_FAST
     return;

@@ -392,6 +392,19 @@ def test_tree_attention_edge_cases():
         check_close(down16(out), ref, f"attention {cfg.name}")
 
 
+@pytest.mark.parametrize("shape,P,T", [("1b", 16391, 64), ("8b", 16400, 33), ("70b", 16384, 17)])
+def test_tree_attention_long_prefix_eight_wave_workgroups(shape, P, T):
+    """More than 128 query rows per KV head and a prefix that may reach 16K
+    keys: workgroups of 8 waves (256 rows), one per compute unit, 32 parts;
+    prefixes not a multiple of the 32-key stage, trees of 17 to 64 nodes."""
+    from gen.workloads import WorkloadConfig
+    sh = {"1b": LLAMA_1B, "8b": LLAMA_8B, "70b": LLAMA_70B}[shape]
+    cfg = WorkloadConfig(70 + T, f"long-{shape}", sh, P=P, T=T, levels=min(T, 9), branching=3)
+    out, dkc, dvc, ref, okc, ovc = _attn_case(cfg, seed=cfg.index)
+    check_close(down16(out), ref, f"attention {cfg.name}")
+    check_close(down16(dkc)[:, P:P + T], okc[:, P:P + T], "rotated tree keys")
+
+
 def test_tree_attention_non_ancestor_perturbation_is_bitwise_invisible():
     cfg = CONFIGS["c2"]
     s = cfg.shape

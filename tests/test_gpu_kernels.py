@@ -220,6 +220,40 @@ def test_w4a16_gemm_deterministic_and_split_consistent():
     check_close(outs[0], oracle.w4a16_gemm(W, x), "gemm det")
 
 
+@pytest.mark.parametrize("M,K,N,swiglu", [(32, 8192, 10240, False), (13, 2048, 4096, False), (64, 4096, 14336, True)])
+def test_w4a16_split_blocks_reuse_one_workspace(M, K, N, swiglu):
+    """Column blocks split between workgroups (partials summed in workgroup
+    order): five calls on one workspace give bit-identical results within
+    tolerance of the oracle and leave the workspace header zero."""
+    W = _rand_w4(17, N, K)
+    t, d = upload_w4(W)
+    x = gen.normal_f16(17, 1, (M, K))
+    dx = up(x)
+    if swiglu:
+        Wu = _rand_w4(18, N, K)
+        tu, du = upload_w4(Wu)
+        ws = ss.workspace(ss.swiglu_workspace_bytes(M, K, N), dev())
+        ref = oracle.w4a16_swiglu(W, Wu, x)
+    else:
+        r = gen.normal_f16(17, 2, (M, N))
+        ws = ss.workspace(ss.gemm_workspace_bytes(M, K, N), dev())
+        ref = oracle.w4a16_gemm(W, x, residual=r)
+    outs = []
+    for _ in range(5):
+        dy = torch.zeros((M, N), dtype=torch.int16, device=dev())
+        if swiglu:
+            ss.w4a16_swiglu(d, du, dx, dy, ws)
+        else:
+            ss.w4a16_gemm(d, dx, dy, ws, residual=up(r))
+        torch.cuda.synchronize()
+        outs.append(down16(dy))
+        header = ws[:ss.WS_HEADER_BYTES].cpu().numpy()
+        assert not header.any(), "workspace header not left zero"
+    for o in outs[1:]:
+        assert np.array_equal(outs[0], o)
+    check_close(outs[0], ref, f"split blocks M={M} K={K} N={N}")
+
+
 @pytest.mark.parametrize("name", ["c1", "c3"])
 def test_w4a16_swiglu_config_shapes(name):
     cfg = CONFIGS[name]

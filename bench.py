@@ -15,8 +15,11 @@ Prints one JSON line: value = mean microseconds per layer (lower is better)
 with p10/p50/p90 over the replays; per-operation standalone timings with
 algorithmic bytes and achieved GB/s (GEMMs with their split-K fix-up,
 attention with its merge); the roofline of the dominant operation (the
-fused SwiGLU W4A16 GEMM) timed on its own stream with HIP events; and the
-fp64 CPU reference checker timed on the host as a baseline.
+fused SwiGLU W4A16 GEMM) timed on its own stream with HIP events; the same
+per-layer figures (fewer replays) for the other layer configurations
+(`configs`: 1B, 8B, 8B at a 32K prefix); and the fp64 CPU reference checker
+timed on the host as a baseline (all threads and one thread, median of
+three runs each).
 """
 import argparse
 import hashlib
@@ -40,6 +43,9 @@ def parse():
     ap.add_argument("--config", default="c3")
     ap.add_argument("--copies", type=int, default=0, help="layer copies rotated (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-repeats", type=int, default=3, help="runs of each CPU-baseline leg (median)")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the per-layer sub-results of the other layer configurations (c1, c2, c4)")
     ap.add_argument("--only-kernel", default="", help="launch only this kernel (for counter runs): "
                     "swiglu | qkv | o | down | attention | commit | copy")
     ap.add_argument("--iters", type=int, default=50)
@@ -90,27 +96,13 @@ def read_traffic(kernel_tag, cur_hash):
         return None
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); sharding across GPUs "
-              "is not implemented.", file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
-    import torch
-
-    import paper_2506_11309_amd as ss
+def setup_layers(cfg_name, args, ss, torch, np, dev):
+    """Seeded synthetic inputs of one layer configuration, uploaded: enough
+    layer copies (weights and KV cache) to defeat the Infinity Cache."""
     from gen import workloads as wl
-
-    if not os.path.exists(ss.LIB_PATH):
-        import __graft_entry__
-        __graft_entry__.build()
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    cfg = wl.CONFIGS[args.config]
+    cfg = wl.CONFIGS[cfg_name]
     s = cfg.shape
     T = cfg.T
-
     t0 = time.time()
     w = wl.make_layer_weights(cfg)
     kc, vc = wl.make_kv_prefix(cfg)
@@ -126,7 +118,6 @@ def main():
 
     layer_bytes = s.w4_bytes() + cfg.kv_bytes_per_layer()
     copies = args.copies or max(2, -(-2 * MALL_BYTES // layer_bytes) + 1)
-    stream = torch.cuda.Stream()
     dims = ss.make_dims(s.H, s.Hq, s.Hkv, s.D, s.F, cfg.S_max)
     rope = up(ss.rope_table(500000.0, cfg.S_max, s.D))
     dparent = up(parent)
@@ -148,46 +139,12 @@ def main():
         d["ws"] = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
         inst.append(d)
     torch.cuda.synchronize()
+    return {"cfg": cfg, "s": s, "T": T, "w": w, "kc": kc, "vc": vc, "x": x, "parent": parent, "acc": acc,
+            "gen_s": gen_s, "copies": copies, "dims": dims, "rope": rope, "dparent": dparent, "dacc": dacc,
+            "kc_all": kc_all, "vc_all": vc_all, "P_dev": P_dev, "inst": inst, "up": up}
 
-    if args.gemm_ab:
-        gemm_ab(ss, torch, np, inst, cfg, stream, dev)
-        return
 
-    # ---------------- counter-run mode: one kernel type only ----------------
-    if args.only_kernel:
-        run_only(args, ss, torch, np, inst, cfg, dims, dparent, dacc, rope, stream, dev)
-        return
-
-    # ---------------- step graph: every layer copy once, in order ----------------
-    # (like a multi-layer model step; the per-layer value is the step time
-    # divided by the number of layers)
-    step = ss.Graph()
-    with torch.cuda.stream(stream):
-        step.begin(stream)
-        for d in inst:
-            ss.verify_layer(d["layer"], dims, d["h"], d["P"], dparent, rope, d["ws"], stream=stream)
-        step.end(stream)
-        for i in range(args.warmup):
-            step.launch(stream)
-    stream.synchronize()
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    with torch.cuda.stream(stream):
-        ev[0].record(stream)
-        for i in range(args.steps):
-            step.launch(stream)
-            ev[i + 1].record(stream)
-    ev[-1].synchronize()
-    torch.cuda.synchronize()
-    ms_total = ev[0].elapsed_time(ev[-1])
-    ms_step = ms_total / args.steps / copies  # per layer
-    per = sorted(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / copies for i in range(args.steps))
-    pct = lambda q: round(per[min(len(per) - 1, int(q * len(per)))], 3)
-    for d in inst:
-        err = ss.read_device_error(d["ws"], stream)
-        if err:
-            raise RuntimeError(f"device error word {err}")
-
+def make_time_op(ss, torch, stream):
     def time_op(fn, iters):
         """Mean microseconds of one fn(i) call: `iters` calls (rotating layer
         copies) captured into a HIP graph, replayed 3 times, timed with HIP
@@ -208,22 +165,54 @@ def main():
             e1.record(stream)
         e1.synchronize()
         return e0.elapsed_time(e1) * 1000.0 / (3 * iters)
+    return time_op
 
-    # ---------------- KV commit: all layer copies in one launch ----------------
-    cm_ws = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
-    commit_us = time_op(lambda i: ss.kv_commit(kc_all, vc_all, P_dev, dparent, dacc, n_layers=copies,
-                                               advance=False, ws=cm_ws, stream=stream), 50)
-    if ss.read_device_error(cm_ws, stream):
-        raise RuntimeError("device error in kv_commit")
 
-    # ---------------- per-operation standalone timings ----------------
-    it = max(args.steps // 2, 30)
+def time_step(ctx, steps, warmup, ss, torch, stream):
+    """The step graph (every layer copy once, in order, like a multi-layer
+    model step) replayed `steps` times after `warmup` replays; per-layer
+    microseconds of each replay."""
+    inst, copies = ctx["inst"], ctx["copies"]
+    step = ss.Graph()
+    with torch.cuda.stream(stream):
+        step.begin(stream)
+        for d in inst:
+            ss.verify_layer(d["layer"], ctx["dims"], d["h"], d["P"], ctx["dparent"], ctx["rope"], d["ws"],
+                            stream=stream)
+        step.end(stream)
+        for i in range(warmup):
+            step.launch(stream)
+    stream.synchronize()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    with torch.cuda.stream(stream):
+        ev[0].record(stream)
+        for i in range(steps):
+            step.launch(stream)
+            ev[i + 1].record(stream)
+    ev[-1].synchronize()
+    torch.cuda.synchronize()
+    ms_total = ev[0].elapsed_time(ev[-1])
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / copies for i in range(steps))
+    for d in inst:
+        err = ss.read_device_error(d["ws"], stream)
+        if err:
+            raise RuntimeError(f"device error word {err}")
+    return ms_total / steps / copies, per
+
+
+def time_ops(ctx, it, ss, torch, stream, dev):
+    """Standalone timings of the layer's operations (GEMMs with their split-K
+    fix-up, attention with its merge), algorithmic bytes, GB/s."""
+    s, T, copies, inst = ctx["s"], ctx["T"], ctx["copies"], ctx["inst"]
+    cfg = ctx["cfg"]
+    time_op = make_time_op(ss, torch, stream)
     w4b = lambda K, N: K * N // 2 + (K // 128) * N * 3
-    xin = up(x)
+    xin = ctx["up"](ctx["x"])
     big_x = torch.zeros((T, max(s.H, s.F, s.Hq * s.D)), dtype=torch.int16, device=dev)
     big_x.copy_(torch.randint(-3000, 3000, big_x.shape, dtype=torch.int16, device=dev) & 0x3BFF)
     y = torch.zeros((T, max(s.F, s.n_qkv)), dtype=torch.int16, device=dev)
-    op_ws = ss.workspace(ss.verify_layer_workspace_bytes(dims, T), dev)
+    op_ws = ss.workspace(ss.verify_layer_workspace_bytes(ctx["dims"], T), dev)
     preps = {K: torch.zeros(ss.prepared_bytes(T, K), dtype=torch.uint8, device=dev) for K in {s.H, s.F, s.Hq * s.D}}
     with torch.cuda.stream(stream):
         for K, xp in preps.items():
@@ -245,8 +234,9 @@ def main():
     Hd = s.Hq * s.D
     qkv_t = big_x[:, :s.n_qkv] if s.n_qkv <= big_x.shape[1] else None
     att_us = time_op(lambda i: ss.tree_attention(qkv_t, qkv_t[:, Hd:], qkv_t[:, Hd + s.Hkv * s.D:],
-                                                 inst[i % copies]["kc"], inst[i % copies]["vc"], P_dev, dparent,
-                                                 s.Hq, s.Hkv, s.D, rope, y[:, :Hd], op_ws, stream=stream), it)
+                                                 inst[i % copies]["kc"], inst[i % copies]["vc"], ctx["P_dev"],
+                                                 ctx["dparent"], s.Hq, s.Hkv, s.D, ctx["rope"], y[:, :Hd], op_ws,
+                                                 stream=stream), it)
     att_bytes = 2 * s.Hkv * (cfg.P + T) * s.D * 2 + T * (s.n_qkv + Hd) * 2
     ops["attention"] = {"us": round(att_us, 3), "bytes": att_bytes}
     rn_us = time_op(lambda i: ss.rmsnorm(xin, inst[0]["an"], y[:, :s.H], stream=stream), it)
@@ -259,32 +249,156 @@ def main():
     g_us = sum(ops[n]["us"] for n in g_names)
     gemm_agg = {"bytes": g_bytes, "us": round(g_us, 3), "GBps": round(g_bytes / (g_us * 1e-6) / 1e9, 1),
                 "frac_hbm": round(g_bytes / (g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    return ops, gemm_agg
+
+
+def workload_label(cfg):
+    s = cfg.shape
+    return (f"{cfg.name}: {SHAPE_LABEL.get(s.H, 'Llama')}-shaped layer, H={s.H}, Hq/Hkv={s.Hq}/{s.Hkv}, "
+            f"D={s.D}, F={s.F}, int4 g128; tree T={cfg.T} ({cfg.levels} levels, branching<={cfg.branching}); "
+            f"prefix P={cfg.P}")
+
+
+def other_config(name, args, ss, torch, np, dev, stream):
+    """Per-layer latency, GEMM aggregate and attention bandwidth of another
+    layer configuration (fewer replays than the headline configuration)."""
+    ctx = setup_layers(name, args, ss, torch, np, dev)
+    ms, per = time_step(ctx, max(args.steps // 4, 20), max(args.warmup // 2, 5), ss, torch, stream)
+    ops, gagg = time_ops(ctx, max(args.steps // 8, 20), ss, torch, stream, dev)
+    out = {"workload": workload_label(ctx["cfg"]), "us_per_layer": round(ms * 1000.0, 3),
+           "us_per_layer_p50": round(per[len(per) // 2], 3), "layer_copies_rotated": ctx["copies"],
+           "gemm_aggregate": gagg, "attention": ops["attention"],
+           "ops_us": {k: v["us"] for k, v in ops.items()}}
+    del ctx
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(ctx, args):
+    """The fp64 reference checker on the host: the whole layer step (+ KV
+    commit), with every thread it is given and with one thread; median of
+    `args.cpu_repeats` runs each (progress on stderr)."""
+    import oracle
+    cfg, s, w, x = ctx["cfg"], ctx["s"], ctx["w"], ctx["x"]
+    odims = {"H": s.H, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "F": s.F, "S_max": cfg.S_max}
+    threads_all = oracle.num_threads()
+
+    def run(reps, label):
+        times = []
+        for r in range(reps):
+            okc, ovc = ctx["kc"].copy(), ctx["vc"].copy()
+            t1 = time.time()
+            oracle.verify_layer(odims, w, okc, ovc, x, cfg.P, ctx["parent"])
+            oracle.kv_commit(okc, ovc, cfg.P, ctx["parent"], ctx["acc"])
+            times.append(time.time() - t1)
+            print(f"cpu baseline ({label}) run {r + 1}/{reps}: {times[-1]:.2f} s", file=sys.stderr, flush=True)
+        return times
+
+    reps = max(1, args.cpu_repeats)
+    all_t = run(reps, f"{threads_all} threads")
+    oracle.set_num_threads(1)
+    try:
+        one_t = run(reps, "1 thread")
+    finally:
+        oracle.set_num_threads(threads_all)
+    med = lambda v: sorted(v)[len(v) // 2]
+    sample = f"one full {cfg.name} layer step (T={cfg.T}, P={cfg.P}) + KV commit, fp64"
+    return {"value": round(med(all_t) * 1e6, 1), "unit": "us/layer", "cores": threads_all, "kind": "oracle",
+            "sample": f"{sample}, {threads_all} OpenMP threads; median of {reps} runs",
+            "repeats_s": [round(t, 3) for t in all_t],
+            "single_thread": {"value": round(med(one_t) * 1e6, 1), "unit": "us/layer", "cores": 1,
+                              "sample": f"{sample}, 1 thread; median of {reps} runs",
+                              "repeats_s": [round(t, 3) for t in one_t]},
+            "cpu_model": cpu_model(), "host_cpus_visible": len(os.sched_getaffinity(0))}
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); sharding across GPUs "
+              "is not implemented.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2506_11309_amd as ss
+
+    if not os.path.exists(ss.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream()
+    ctx = setup_layers(args.config, args, ss, torch, np, dev)
+    cfg, s, T, copies, inst = ctx["cfg"], ctx["s"], ctx["T"], ctx["copies"], ctx["inst"]
+    log(f"{args.config}: {copies} layer copies uploaded")
+
+    if args.gemm_ab:
+        gemm_ab(ss, torch, np, inst, cfg, stream, dev)
+        return
+
+    # ---------------- counter-run mode: one kernel type only ----------------
+    if args.only_kernel:
+        run_only(args, ss, torch, np, inst, cfg, ctx["dims"], ctx["dparent"], ctx["dacc"], ctx["rope"], stream, dev)
+        return
+
+    # ---------------- step graph: every layer copy once, in order ----------------
+    ms_step, per = time_step(ctx, args.steps, args.warmup, ss, torch, stream)
+    log(f"step: {ms_step * 1000.0:.1f} us/layer")
+    pct = lambda q: round(per[min(len(per) - 1, int(q * len(per)))], 3)
+    time_op = make_time_op(ss, torch, stream)
+
+    # ---------------- KV commit: all layer copies in one launch ----------------
+    cm_ws = ss.workspace(ss.verify_layer_workspace_bytes(ctx["dims"], T), dev)
+    commit_us = time_op(lambda i: ss.kv_commit(ctx["kc_all"], ctx["vc_all"], ctx["P_dev"], ctx["dparent"],
+                                               ctx["dacc"], n_layers=copies, advance=False, ws=cm_ws,
+                                               stream=stream), 50)
+    if ss.read_device_error(cm_ws, stream):
+        raise RuntimeError("device error in kv_commit")
+
+    # ---------------- per-operation standalone timings ----------------
+    ops, gemm_agg = time_ops(ctx, max(args.steps // 2, 30), ss, torch, stream, dev)
+    log("per-operation timings done")
 
     # ---------------- dominant operation: fused SwiGLU GEMM ----------------
+    sw_us = ops["swiglu"]["us"]
     sw_bytes = ops["swiglu"]["bytes"]
     sw_gbs = sw_bytes / (sw_us * 1e-6) / 1e9
     # the counter profile was taken on the 70B layer (c3): other shapes report none
     traffic = read_traffic("swiglu_gemm_c3", source_hash(GEMM_SOURCES)) if args.config == "c3" else None
 
     full = None if args.no_full_step else full_step(args, ss, torch, np, dev, stream)
+    log("80-layer step done")
     draft = None if args.no_draft_side else draft_side(args, ss, torch, np, dev, stream)
     shard = None if args.no_paper_shard else paper_shard(args, ss, torch, np, dev, stream)
+    log("draft side and TP4 shard done")
     loop = None if args.no_tree_loop else tree_loop(ss, torch, np, dev, stream)
+    log("tree loop done")
+    others = {}
+    if not args.no_other_configs:
+        for name in ("c1", "c2", "c4"):
+            if name != args.config:
+                others[name] = other_config(name, args, ss, torch, np, dev, stream)
+                log(f"{name}: {others[name]['us_per_layer']:.1f} us/layer")
 
     # ---------------- CPU baseline: the fp64 reference checker ----------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        import oracle
-        odims = {"H": s.H, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "F": s.F, "S_max": cfg.S_max}
-        okc, ovc = kc.copy(), vc.copy()
-        t1 = time.time()
-        oracle.verify_layer(odims, w, okc, ovc, x, cfg.P, parent)
-        oracle.kv_commit(okc, ovc, cfg.P, parent, acc)
-        cpu_s = time.time() - t1
-        cpu = {"value": round(cpu_s * 1e6, 1), "unit": "us/layer", "cores": oracle.num_threads(),
-               "kind": "oracle",
-               "sample": f"one full {cfg.name} layer step (T={T}, P={cfg.P}) + commit, fp64, "
-                         f"{oracle.num_threads()} OpenMP threads, timed once"}
+    cpu = None if args.no_cpu_baseline else cpu_baseline(ctx, args)
 
     step_bytes = s.w4_bytes() + cfg.kv_bytes_per_layer()
     out = {
@@ -300,11 +414,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f16 (int4 weights, fp32 accumulate)",
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {SHAPE_LABEL.get(s.H, 'Llama')}-shaped layer, H={s.H}, "
-                               f"Hq/Hkv={s.Hq}/{s.Hkv}, "
-                               f"D={s.D}, F={s.F}, int4 g128; tree T={T} ({cfg.levels} levels, "
-                               f"branching<={cfg.branching}); prefix P={cfg.P}; verify_layer per step, "
-                               f"KV commit timed separately",
+        "config": {"workload": workload_label(cfg) + "; verify_layer per step, KV commit timed separately",
                    "global_batch": T, "seq_len": cfg.P + T, "parallelism": "none (1 GPU)",
                    "layer_copies_rotated": copies, "layers_per_step": copies},
         "us_per_layer_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
@@ -318,11 +428,12 @@ def main():
                      "frac": round(sw_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": sw_bytes, "avg_launch_us": round(sw_us, 3)},
         "cpu_baseline": cpu,
+        "configs": others or None,
         "full_step_80_layers": full,
         "draft_side": draft,
         "paper_tp4_shard": shard,
         "tree_loop": loop,
-        "input_generation_s": round(gen_s, 2),
+        "input_generation_s": round(ctx["gen_s"], 2),
     }
     print(json.dumps(out), flush=True)
 

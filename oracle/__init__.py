@@ -75,6 +75,8 @@ def _load():
     lib.oracle_topk_logprobs.restype = i32
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     _lib = lib
     return lib
 
@@ -312,3 +314,9 @@ def topk_logprobs(logits, k):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the checker's later parallel loops (timing only; every
+    result is independent of the thread count)."""
+    _load().oracle_set_num_threads(int(n))

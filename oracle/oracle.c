@@ -23,6 +23,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads of later parallel regions (timing only: results do not depend on it). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ---------------------------------------------------------------- binary16 */
 
 double oracle_f16_to_f64(uint16_t h) {

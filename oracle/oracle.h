@@ -168,6 +168,7 @@ int32_t oracle_topk_logprobs(const uint16_t* logits, int32_t n, int32_t V, int32
                              int32_t* tokens, double* logprobs);
 
 int oracle_num_threads(void);
+void oracle_set_num_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -145,7 +145,7 @@ size_t swiftspec_w4a16_gemm_valu_workspace_bytes(int32_t M, int32_t K, int32_t N
 
 /* Activations in the matrix-core operand order the GEMMs read
  * ("prepared" layout: [ceil(M/16)][K/128][4][64][8] fp16, rows >= M zero,
- * even k of every 32-wide slice stored times 16).  Chained GEMMs can keep
+ * values as given).  Chained GEMMs can keep
  * activations in this form and call the *_prepared entry points. */
 size_t swiftspec_prepared_bytes(int32_t M, int32_t K);
 int swiftspec_prepare_activations(const uint16_t* x, int32_t M, int32_t ldx, int32_t K, uint16_t* xp,

@@ -143,6 +143,37 @@ __device__ __forceinline__ uint32_t buffer_load_x1(__amdgpu_buffer_rsrc_t r, uin
   return __builtin_amdgcn_raw_buffer_load_b32(r, voffset, soffset, 0);
 }
 
+// 16-byte buffer load of every lane straight into LDS: lane l's 16 bytes
+// (at voff + soff of the buffer) land at LDS address lds_addr + 16 l.  M0,
+// which holds the LDS base of such loads, is saved and restored around the
+// load (one wait state after setting it), so the compiler's own use of M0 is
+// untouched.  The compiler does not see the LDS write: the caller waits for
+// it with vmcnt and orders it against LDS reads with barriers.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 raw_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  return i32x4{(int)(uint32_t)b, (int)(uint32_t)(b >> 32), (int)bytes, 0x00020000};
+}
+__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %4\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, %3 offen lds\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(rsrc), "s"(soff), "s"(lds_addr)
+      : "memory");
+}
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding;
+// expcnt and lgkmcnt are left alone.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 // Ticket for the deterministic "last arriving workgroup combines" pattern,
 // taken by the lane that stored the workgroup's partial.  Acquire-release at
 // agent scope: the release publishes that lane's earlier stores (every

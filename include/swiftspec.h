@@ -181,7 +181,9 @@ int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, cons
  * Node i at position P + depth(i) attends to cache rows [0, P) and to the
  * tree rows P + j of its ancestors-or-self j; query head h reads kv head
  * h / (Hq / Hkv).  1 <= T <= 64, D in {64, 128}, Hq % Hkv == 0,
- * softmax_scale > 0 and finite (SWIFTSPEC_INVALID_ARG otherwise).  An invalid
+ * softmax_scale > 0 and finite (SWIFTSPEC_INVALID_ARG otherwise); q, k, v
+ * and the cache rows read must be finite (NaN or infinite entries give
+ * undefined results, not an error).  An invalid
  * tree or prefix length sets the device error word; then out and the cache
  * are left untouched. */
 int swiftspec_tree_attention(const uint16_t* q, int32_t ldq, const uint16_t* k, const uint16_t* v,

@@ -618,8 +618,8 @@ struct FastAttnCfg {
   static_assert((2 * KvLds<D>::kBlocks) % W == 0, "stage split");
 };
 
-template <int D, int W>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ? 2 : 1))) void tree_attention_fast_kernel(AttnArgs a) {
+template <int D, int W, int TPW>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W * TPW >= 8 ? 2 : 1))) void tree_attention_fast_kernel(AttnArgs a) {
   using L = KvLds<D>;
   using Cfg = FastAttnCfg<D, W>;
   constexpr int NS = Cfg::kStages;
@@ -627,7 +627,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   constexpr int KS = D / 32;   // k-steps of the QK^T product
   constexpr int DT = D / 16;   // d tiles of the PV product
   constexpr int HALF = D / 2;
-  constexpr int VW = 2 * W;    // 16-row virtual waves of the partial layout
+  constexpr int VW = TPW * W;  // 16-row virtual waves of the partial layout
   __shared__ __attribute__((aligned(16))) char kvs[NS * L::kStage];
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -645,12 +645,12 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   // for all nodes), the rotary rows at P + depth, issued ahead of the first
   // key and value stages so that waiting for them leaves those in flight ----
   const int par = lane < a.T ? a.parent[lane] : -1;
-  int node[2], qhead[2];
-  bool row_ok[2];
-  u32x4 qraw[2][KS];
+  int node[TPW], qhead[TPW];
+  bool row_ok[TPW];
+  u32x4 qraw[TPW][KS];
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
-    const int row = rb * (32 * W) + wave * 32 + t2 * 16 + n16;
+  for (int t2 = 0; t2 < TPW; ++t2) {
+    const int row = rb * (16 * VW) + wave * (16 * TPW) + t2 * 16 + n16;
     row_ok[t2] = row < a.R;
     node[t2] = row_ok[t2] ? row / a.G : 0;
     qhead[t2] = g * a.G + (row_ok[t2] ? row % a.G : 0);
@@ -692,10 +692,10 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     vm_wait<0>();
     return;
   }
-  uint64_t anc[2];
-  u32x4 csraw[2][KS / 2][4];  // cos/sin pairs of dimensions 32 j + 8 kq + 0..7
+  uint64_t anc[TPW];
+  u32x4 csraw[TPW][KS / 2][4];  // cos/sin pairs of dimensions 32 j + 8 kq + 0..7
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
+  for (int t2 = 0; t2 < TPW; ++t2) {
     anc[t2] = shfl_u64(anc_all, node[t2]);
     const int dep = __shfl(depth_all, node[t2], kWave);
     const float* cs = a.rope + (size_t)(P + dep) * D;  // [D/2][2]
@@ -742,9 +742,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
 
   // ---- this wave's 32 query rows (tiles t2 = 0, 1): rotated Q as B fragments ----
   const float c2 = a.scale_log2;
-  half8 qf[2][KS];
+  half8 qf[TPW][KS];
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
+  for (int t2 = 0; t2 < TPW; ++t2) {
     float qv[KS][8];
 #pragma unroll
     for (int j = 0; j < KS; ++j) {
@@ -784,10 +784,12 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
   // the reference exponent m_ref and the rescale threshold thr (m_ref +
   // kLazyRescale once the row has seen a key, -inf before); output and row-sum
   // accumulators (O layout: rows 4 kq + r, column n16)
-  float m_ref[2] = {0.f, 0.f}, thr[2] = {-INFINITY, -INFINITY};
-  f32x4 o[2][DT], ol[2];
+  float m_ref[TPW], thr[TPW];
+  f32x4 o[TPW][DT], ol[TPW];
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
+  for (int t2 = 0; t2 < TPW; ++t2) {
+    m_ref[t2] = 0.f;
+    thr[t2] = -INFINITY;
     ol[t2] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[t2][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -811,7 +813,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     constexpr bool kMask = decltype(mask_tag)::value;
     constexpr bool kTree = decltype(tree_tag)::value;
     // S^T: lane holds keys 16 h + 4 kq + r (h < 2, r < 4) of query row n16
-    f32x4 s[2][2];
+    f32x4 s[TPW][2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       half8 kf[KS];
@@ -819,7 +821,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
       for (int j = 0; j < KS; ++j)
         kf[j] = *reinterpret_cast<const half8*>(sb + k_base + (16 * h / L::kRpb) * L::kKStride + 64 * j);
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
+      for (int t2 = 0; t2 < TPW; ++t2) {
         f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < KS; ++j) c = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[j], qf[t2][j], c, 0, 0, 0);
@@ -827,9 +829,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
       }
     }
     // this lane's largest score of each tile (masked keys -inf)
-    float lm[2];
+    float lm[TPW];
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
+    for (int t2 = 0; t2 < TPW; ++t2) {
       if constexpr (kMask) {
 #pragma unroll
         for (int h = 0; h < 2; ++h)
@@ -847,9 +849,11 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     // move a row's reference up only when one of its scores exceeds it by
     // more than 2^8 (the probabilities then stay below 256), and set it at
     // the row's first key (scores scale by c2 > 0, so maxima commute with it)
-    if (__any(lm[0] * c2 > thr[0] || lm[1] * c2 > thr[1])) {
+    bool raise = lm[0] * c2 > thr[0];
+    if constexpr (TPW == 2) raise = raise || lm[1] * c2 > thr[1];
+    if (__any(raise)) {
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
+      for (int t2 = 0; t2 < TPW; ++t2) {
         const float rmax = quarter_reduce(lm[t2], [](float x, float y) { return fmaxf(x, y); }) * c2;
         const bool seen = thr[t2] != -INFINITY;
         const float mn = seen ? fmaxf(m_ref[t2], rmax) : (rmax == -INFINITY ? m_ref[t2] : rmax);
@@ -868,9 +872,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
     }
     // probabilities 2^(c2 s - m_ref) <= 2^8 as the fp16 A fragment: slot
     // 8 kq + 4 h + r holds key 16 h + 4 kq + r
-    half8 pf[2];
+    half8 pf[TPW];
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
+    for (int t2 = 0; t2 < TPW; ++t2) {
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -891,7 +895,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
       const half8 vf = bitcast<half8>(u32x4{bitcast<u32x2>(hv[0])[0], bitcast<u32x2>(hv[0])[1],
                                             bitcast<u32x2>(hv[1])[0], bitcast<u32x2>(hv[1])[1]});
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) o[t2][dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[t2], vf, o[t2][dt], 0, 0, 0);
+      for (int t2 = 0; t2 < TPW; ++t2) o[t2][dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[t2], vf, o[t2][dt], 0, 0, 0);
     }
   };
 
@@ -964,8 +968,8 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
 
   // ---- publish this split's partial (merged by the next kernel) ----
 #pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
-    const int vw = 2 * wave + t2;
+  for (int t2 = 0; t2 < TPW; ++t2) {
+    const int vw = TPW * wave + t2;
     float inv[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) inv[r] = ol[t2][r] > 0.f ? 1.0f / ol[t2][r] : 0.f;
@@ -989,6 +993,17 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ?
 // prefix may reach 16K keys, where streaming the cache dominates
 static int fast_attn_waves(int R, int P_max) {
   return R <= 32 ? 1 : R <= 64 ? 2 : (R <= 128 || P_max < 16384) ? 4 : 8;
+}
+// 16-row tiles per wave of the target kernel: one where a head's rows and
+// the prefix splits leave a single 4-wave workgroup per compute unit (the
+// 70B shape: 8 KV heads x 256 rows, 16 parts), so that 8 waves of 16 rows
+// each give every SIMD two waves over the same 128 rows and LDS stages;
+// else two (32 rows per wave)
+static int fast_attn_tiles(int R, int P_max, int Hkv, int nsplit) {
+  const int W = fast_attn_waves(R, P_max);
+  if (W != 4) return 2;
+  const int RB = (R + 127) / 128;
+  return (long)Hkv * RB * (nsplit + 1) <= 256 ? 1 : 2;
 }
 
 static int attn_waves(int R) { return R >= 128 ? 8 : 4; }
@@ -1055,16 +1070,17 @@ void launch_tree_attention(const AttnLaunch& L, hipStream_t st) {
   if (!draft) {
     // target model: direct-to-LDS kernel, 32 rows per wave, partials in
     // 16-row virtual waves (2 per wave) for the merge kernel
-    const int W = fast_attn_waves(a.R, a.S_max - a.T);
-    a.RB = (a.R + 32 * W - 1) / (32 * W);
+    const int TPW = fast_attn_tiles(a.R, a.S_max - a.T, a.Hkv, a.nsplit);
+    const int W = fast_attn_waves(a.R, a.S_max - a.T) * (2 / TPW);  // waves per workgroup
+    a.RB = (a.R + 16 * TPW * W - 1) / (16 * TPW * W);
     const dim3 grid(L.Hkv * a.RB * (L.nsplit + 1));
-#define SS_FAST(DD, WW)                                                                          \
-    hipLaunchKernelGGL((tree_attention_fast_kernel<DD, WW>), grid, dim3(64 * WW), 0, st, a);     \
-    launch_merge<DD, 2 * WW>(a, st)
+#define SS_FAST(DD, WW, TT)                                                                          \
+    hipLaunchKernelGGL((tree_attention_fast_kernel<DD, WW, TT>), grid, dim3(64 * WW), 0, st, a);         \
+    launch_merge<DD, TT * WW>(a, st)
     if (L.D == 64) {
-      if (W == 1) { SS_FAST(64, 1); } else if (W == 2) { SS_FAST(64, 2); } else if (W == 4) { SS_FAST(64, 4); } else { SS_FAST(64, 8); }
+      if (W == 1) { SS_FAST(64, 1, 2); } else if (W == 2) { SS_FAST(64, 2, 2); } else if (W == 4) { SS_FAST(64, 4, 2); } else if (TPW == 1) { SS_FAST(64, 8, 1); } else { SS_FAST(64, 8, 2); }
     } else {
-      if (W == 1) { SS_FAST(128, 1); } else if (W == 2) { SS_FAST(128, 2); } else if (W == 4) { SS_FAST(128, 4); } else { SS_FAST(128, 8); }
+      if (W == 1) { SS_FAST(128, 1, 2); } else if (W == 2) { SS_FAST(128, 2, 2); } else if (W == 4) { SS_FAST(128, 4, 2); } else if (TPW == 1) { SS_FAST(128, 8, 1); } else { SS_FAST(128, 8, 2); }
     }
 #undef SS_FAST
     return;

@@ -173,8 +173,16 @@ def time_step(ctx, steps, warmup, ss, torch, stream):
     model step) replayed `steps` times after `warmup` replays; per-layer
     microseconds of each replay."""
     inst, copies = ctx["inst"], ctx["copies"]
+    # shader clock sampled on the idle chip, and over the first millisecond
+    # of the timed replays by a one-wave kernel on a second stream (the
+    # power management lowers the clock under load within microseconds and
+    # raises it again as soon as the load stops, so only a sample taken
+    # during the replays shows the clock the kernels run at)
+    clk = torch.zeros(8, dtype=torch.int64, device=inst[0]["h"].device)
+    side = torch.cuda.Stream()
     step = ss.Graph()
     with torch.cuda.stream(stream):
+        ss.clock_sample(clk[0:4], 20, stream=stream)
         step.begin(stream)
         for d in inst:
             ss.verify_layer(d["layer"], ctx["dims"], d["h"], d["P"], ctx["dparent"], ctx["rope"], d["ws"],
@@ -185,13 +193,19 @@ def time_step(ctx, steps, warmup, ss, torch, stream):
     stream.synchronize()
     torch.cuda.synchronize()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    with torch.cuda.stream(side):
+        ss.clock_sample(clk[4:8], 1000, stream=side)
     with torch.cuda.stream(stream):
         ev[0].record(stream)
         for i in range(steps):
             step.launch(stream)
             ev[i + 1].record(stream)
     ev[-1].synchronize()
+    side.synchronize()
     torch.cuda.synchronize()
+    c = clk.cpu().tolist()
+    ctx["clock_ghz"] = {"idle_before_warmup": round(ss.clock_ghz(c[0:4]), 3),
+                        "during_timed_steps": round(ss.clock_ghz(c[4:8]), 3)}
     ms_total = ev[0].elapsed_time(ev[-1])
     per = sorted(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / copies for i in range(steps))
     for d in inst:
@@ -418,6 +432,9 @@ def main():
                    "global_batch": T, "seq_len": cfg.P + T, "parallelism": "none (1 GPU)",
                    "layer_copies_rotated": copies, "layers_per_step": copies},
         "us_per_layer_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
+        "shader_clock_ghz": dict(ctx["clock_ghz"], nominal=2.4,
+                                 how="s_memtime over s_memrealtime in a one-wave kernel: 20 us on the idle "
+                                     "chip; 1 ms on a second stream at the start of the timed replays"),
         "step_hbm_gbs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "kv_commit_us": {"all_layers": round(commit_us, 3), "layers": copies,
                          "per_layer": round(commit_us / copies, 3)},

@@ -487,6 +487,22 @@ int swiftspec_verify_step(const swiftspec_layer* layers, int32_t n_layers, const
                           uint16_t* logits, void* ws, size_t ws_bytes, void* stream);
 size_t swiftspec_verify_step_workspace_bytes(const swiftspec_dims* dims, int32_t T, int32_t V);
 
+/* -------------------------------------------------------- clock sample
+ * Measurement helper for benchmarks, not part of the verification path.
+ * Enqueues on `stream` one single-wave kernel.  The kernel reads the shader
+ * clock counter (s_memtime) and the 100 MHz real-time counter
+ * (s_memrealtime).  It then polls until the real-time counter has advanced
+ * by window_us microseconds (1..1000; it also stops after 2^22 polls), and
+ * reads both counters again.  The four 64-bit values go to d_out[0..3]
+ * (caller-owned device memory, 8-byte aligned): shader start, real start,
+ * shader end, real end.  The shader clock in GHz is
+ * (d_out[2] - d_out[0]) / (d_out[3] - d_out[1]) / 10.  Enqueued right
+ * after a timed region, it reports the clock the chip held there (the
+ * power management changes clocks over milliseconds, not microseconds).
+ * Returns INVALID_ARG for a null or misaligned d_out or a window outside
+ * 1..1000. */
+int swiftspec_clock_sample(uint64_t* d_out, int32_t window_us, void* stream);
+
 /* ---------------------------------------------------------- HIP graphs
  * Capture the calls issued on `stream` between begin and end into an
  * executable graph (hipStreamBeginCapture / hipGraphInstantiate) and replay

@@ -77,6 +77,7 @@ _SIGS = {
     "swiftspec_greedy_accept_workspace_bytes": ([i32], sz),
     "swiftspec_greedy_accept": ([vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     "swiftspec_read_device_error": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
+    "swiftspec_clock_sample": ([vp, i32, vp], ctypes.c_int),
     "swiftspec_w4_packed_bytes": ([i32, i32], sz),
     "swiftspec_w4_prepack": ([ctypes.POINTER(W4), vp, sz, vp], ctypes.c_int),
     "swiftspec_w4a16_gemm": ([ctypes.POINTER(W4), vp, i32, i32, vp, i32, vp, i32, vp, sz, vp], ctypes.c_int),
@@ -214,6 +215,20 @@ def read_device_error(ws, stream=None) -> int:
     _check(_load().swiftspec_read_device_error(_ptr(ws), _stream(stream), ctypes.byref(out)),
            "read_device_error")
     return int(out.value)
+
+
+def clock_sample(out, window_us: int = 20, stream=None):
+    """Enqueue the clock sample on `stream` into `out` (an int64 device
+    tensor of at least 4 elements): shader-clock and real-time counters
+    before and after a window_us wait."""
+    assert out.numel() >= 4 and out.element_size() == 8
+    _check(_load().swiftspec_clock_sample(_ptr(out), window_us, _stream(stream)), "clock_sample")
+
+
+def clock_ghz(sample) -> float:
+    """Shader clock in GHz from a clock_sample result (host sequence of 4)."""
+    c0, r0, c1, r1 = (int(v) for v in sample[:4])
+    return (c1 - c0) / max(1, r1 - r0) / 10.0
 
 
 def workspace_init(ws, stream=None):

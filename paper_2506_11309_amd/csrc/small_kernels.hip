@@ -337,6 +337,31 @@ void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc
   hipLaunchKernelGGL(tree_masks_kernel, dim3(n_trees), dim3(64), 0, st, parents, T, anc, depth, status);
 }
 
+// -------------------------------------------------------- clock sample
+// One wave: shader-clock and 100 MHz real-time counters before and after a
+// bounded wait of `ticks` real-time ticks.
+__global__ __launch_bounds__(64) void clock_sample_kernel(uint64_t* __restrict__ out, uint32_t ticks) {
+  const uint64_t c0 = __builtin_amdgcn_s_memtime();
+  const uint64_t r0 = __builtin_amdgcn_s_memrealtime();
+  uint64_t r = r0;
+  for (int i = 0; i < (1 << 22) && r - r0 < ticks; ++i) {
+    __builtin_amdgcn_s_sleep(1);
+    r = __builtin_amdgcn_s_memrealtime();
+  }
+  const uint64_t c1 = __builtin_amdgcn_s_memtime();
+  r = __builtin_amdgcn_s_memrealtime();
+  if (threadIdx.x == 0) {
+    out[0] = c0;
+    out[1] = r0;
+    out[2] = c1;
+    out[3] = r;
+  }
+}
+
+void launch_clock_sample(uint64_t* out, uint32_t ticks, hipStream_t st) {
+  hipLaunchKernelGGL(clock_sample_kernel, dim3(1), dim3(64), 0, st, out, ticks);
+}
+
 // ------------------------------------------------------ workspace init
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)

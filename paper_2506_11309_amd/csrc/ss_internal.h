@@ -95,6 +95,7 @@ void launch_kv_commit(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_
 void launch_tree_masks(const int32_t* parents, int n_trees, int T, uint64_t* anc, int32_t* depth,
                        int32_t* status, hipStream_t st);
 
+void launch_clock_sample(uint64_t* out, uint32_t ticks, hipStream_t st);
 void launch_ws_init(void* ws, size_t bytes, hipStream_t st);
 
 void launch_kv_reorganize(uint16_t* k_cache, uint16_t* v_cache, int n_layers, int64_t layer_stride, int Hkv,

@@ -271,6 +271,13 @@ int swiftspec_read_device_error(void* ws, void* stream, uint32_t* out) {
   return hip_status(hipStreamSynchronize(S(stream)));
 }
 
+int swiftspec_clock_sample(uint64_t* d_out, int32_t window_us, void* stream) {
+  if (!d_out || (reinterpret_cast<uintptr_t>(d_out) & 7u) || window_us < 1 || window_us > 1000)
+    return SWIFTSPEC_INVALID_ARG;
+  ss::launch_clock_sample(d_out, (uint32_t)window_us * 100u, S(stream));
+  return check_launch();
+}
+
 size_t swiftspec_w4_packed_bytes(int32_t K, int32_t N) {
   if (K <= 0 || N <= 0) return 0;
   return ss::w4_packed_bytes(K, N);

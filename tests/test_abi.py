@@ -187,3 +187,12 @@ def test_rope_table_is_fp32_rounding_of_fp64_angles(ss):
     ang = pos * inv[None, :]
     assert np.array_equal(t[..., 0], np.cos(ang).astype(np.float32))
     assert np.array_equal(t[..., 1], np.sin(ang).astype(np.float32))
+
+
+def test_clock_sample_rejects_before_launch(ss):
+    lib = ss._load()
+    assert lib.swiftspec_clock_sample(None, 20, None) == ss.INVALID_ARG
+    assert lib.swiftspec_clock_sample(ctypes.c_void_p(8), 0, None) == ss.INVALID_ARG
+    assert lib.swiftspec_clock_sample(ctypes.c_void_p(8), 1001, None) == ss.INVALID_ARG
+    assert lib.swiftspec_clock_sample(ctypes.c_void_p(12), 20, None) == ss.INVALID_ARG
+    assert ss.clock_ghz([1000, 0, 2000, 50]) == 2.0

@@ -420,7 +420,10 @@ def test_tree_attention_edge_cases():
     cases = [WorkloadConfig(61, "e1", LLAMA_8B, P=0, T=5, levels=3, branching=2),
              WorkloadConfig(62, "e2", LLAMA_1B, P=77, T=1, levels=1, branching=1),
              WorkloadConfig(63, "e3", LLAMA_70B, P=130, T=64, levels=64, branching=1),
-             WorkloadConfig(64, "e4", LLAMA_8B, P=1000, T=33, levels=7, branching=4)]
+             WorkloadConfig(64, "e4", LLAMA_8B, P=1000, T=33, levels=7, branching=4),
+             # 104 query rows per KV head in 16-row waves: the 7th wave half
+             # empty, the 8th wholly past the rows
+             WorkloadConfig(65, "e5", LLAMA_70B, P=2000, T=13, levels=5, branching=3)]
     for cfg in cases:
         out, dkc, dvc, ref, okc, ovc = _attn_case(cfg, seed=cfg.index)
         check_close(down16(out), ref, f"attention {cfg.name}")

@@ -22,12 +22,13 @@ struct GemmLaunch {
   int nw;       // N-tiles (16 columns) per block, counting gate and up tiles for SwiGLU
   int nblocks;  // column blocks
   int nwg;      // workgroups launched
+  int ksw;      // > 0: one workgroup per column tile with ksw waves splitting K (no partials)
   bool swiglu;
   float* part;  // split-K partial slots (2 per workgroup)
 };
 
 struct GemmPlan {
-  int nw, nblocks, nwg;
+  int nw, nblocks, nwg, ksw = 0;
   size_t part_bytes;  // split partials
   size_t prep_bytes;  // prepared activations of the input
 };

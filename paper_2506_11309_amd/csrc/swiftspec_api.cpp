@@ -88,6 +88,7 @@ void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* ap
   L.nw = p.nw;
   L.nblocks = p.nblocks;
   L.nwg = p.nwg;
+  L.ksw = p.ksw;
   L.swiglu = swiglu;
   L.part = part;
   ss::launch_w4a16_gemm(L, st);

@@ -97,6 +97,34 @@ constexpr GemmShape gemm_shape_epi(int MT, int EPI) {
 }
 constexpr int kRingL = 3;  // LDS ring of activation fragments
 
+// The four MFMA B operands of one 16-column x 128-k weight block as a lane
+// holds it (16 bytes w: k in [128 g + 32 kq, +32) of column lane % 16; the
+// block's scale|zero word sz), dequantised to exact q - z (see the magic
+// numbers above the loop of w4a16_gemm_kernel): low nibbles of the first
+// and second 16 k, then high nibbles.  magic_lo / magic_hi hold 0x64006400
+// and 0x54005400 in registers.
+struct BFrag {
+  half8 lo_a, lo_b, hi_a, hi_b;
+};
+__device__ __forceinline__ BFrag dequant_block(u32x4 w, uint32_t sz, uint32_t magic_lo, uint32_t magic_hi) {
+  auto deq = [&](uint32_t x, uint32_t m, uint32_t magic, half2v zz) {
+    return bitcast<uint32_t>(bitcast<half2v>((x & m) | (magic & ~m)) - zz);
+  };
+  const uint32_t s0 = w[0] >> 8, s1 = w[1] >> 8, s2 = w[2] >> 8, s3 = w[3] >> 8;
+  constexpr uint32_t kLo = 0x000F000Fu, kHi = 0x00F000F0u;
+  const uint32_t z = (sz >> 16) & 0xFFu;
+  const half2v zlo = bitcast<half2v>((0x6400u + z) * 0x00010001u);
+  const half2v zhi = bitcast<half2v>((0x5400u + 16u * z) * 0x00010001u);
+  auto dl = [&](uint32_t x) { return deq(x, kLo, magic_lo, zlo); };
+  auto dh = [&](uint32_t x) { return deq(x, kHi, magic_hi, zhi); };
+  BFrag f;
+  f.lo_a = bitcast<half8>(u32x4{dl(w[0]), dl(s0), dl(w[1]), dl(s1)});
+  f.lo_b = bitcast<half8>(u32x4{dl(w[2]), dl(s2), dl(w[3]), dl(s3)});
+  f.hi_a = bitcast<half8>(u32x4{dh(w[0]), dh(s0), dh(w[1]), dh(s1)});
+  f.hi_b = bitcast<half8>(u32x4{dh(w[2]), dh(s2), dh(w[3]), dh(s3)});
+  return f;
+}
+
 // Output epilogue of one N-block from the accumulators of wave `wave`
 // (kColW column tiles, for SwiGLU followed by the matching up tiles): lane
 // holds rows 4 * (lane / 16) + r of column lane % 16 of each tile.  The
@@ -256,9 +284,6 @@ void w4a16_gemm_kernel(GemmArgs a) {
   // the mask in a scalar register.
   uint32_t magic_lo = 0x64006400u, magic_hi = 0x54005400u;
   asm volatile("" : "+v"(magic_lo), "+v"(magic_hi));
-  auto deq = [&](uint32_t x, uint32_t m, uint32_t magic, half2v zz) {
-    return bitcast<uint32_t>(bitcast<half2v>((x & m) | (magic & ~m)) - zz);
-  };
   auto read_a = [&](int slot, half8 (&af)[MT][4]) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -272,26 +297,15 @@ void w4a16_gemm_kernel(GemmArgs a) {
                        uint32_t (&sw)[NWV]) {
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) {
-      const u32x4 w = st.b[nt];
-      const uint32_t s0 = w[0] >> 8, s1 = w[1] >> 8, s2 = w[2] >> 8, s3 = w[3] >> 8;
-      constexpr uint32_t kLo = 0x000F000Fu, kHi = 0x00F000F0u;
-      const uint32_t z = (st.sz[nt] >> 16) & 0xFFu;
-      const half2v zlo = bitcast<half2v>((0x6400u + z) * 0x00010001u);
-      const half2v zhi = bitcast<half2v>((0x5400u + 16u * z) * 0x00010001u);
-      auto dl = [&](uint32_t x) { return deq(x, kLo, magic_lo, zlo); };
-      auto dh = [&](uint32_t x) { return deq(x, kHi, magic_hi, zhi); };
-      const half8 blo_a = bitcast<half8>(u32x4{dl(w[0]), dl(s0), dl(w[1]), dl(s1)});
-      const half8 blo_b = bitcast<half8>(u32x4{dl(w[2]), dl(s2), dl(w[3]), dl(s3)});
-      const half8 bhi_a = bitcast<half8>(u32x4{dh(w[0]), dh(s0), dh(w[1]), dh(s1)});
-      const half8 bhi_b = bitcast<half8>(u32x4{dh(w[2]), dh(s2), dh(w[3]), dh(s3)});
+      const BFrag bf = dequant_block(st.b[nt], st.sz[nt], magic_lo, magic_hi);
       sw[nt] = st.sz[nt];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 cc = {0.f, 0.f, 0.f, 0.f};
-        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][0], blo_a, cc, 0, 0, 0);
-        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][1], blo_b, cc, 0, 0, 0);
-        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][2], bhi_a, cc, 0, 0, 0);
-        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][3], bhi_b, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][0], bf.lo_a, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][1], bf.lo_b, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][2], bf.hi_a, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mt][3], bf.hi_b, cc, 0, 0, 0);
         c[mt][nt] = cc;
       }
     }
@@ -510,6 +524,112 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
   ep.write(a, nb, wave, lane, acc);
 }
 
+// ------------------------------------------------- small M, small weights
+// Up to 16 rows and a few megabytes of weights (the 1B-shaped layer's and
+// the 8B-shaped layer's QKV and O projections, tensor-parallel shards) the
+// stream-K kernel's time is its fixed costs: first loads, the split
+// partials and the fix-up kernel.  Here one workgroup owns one 16-column
+// output tile over the whole K range: its W waves take contiguous group
+// ranges, each streaming its own weight blocks and activation fragments
+// (the prepared layout's four fragments of the group, straight into the
+// MFMA A operand) through a 3-deep register ring, and the W partial sums
+// are added in wave order through LDS (results deterministic), then wave 0
+// adds the residual and writes the tile.  No partials leave the workgroup
+// and no second kernel runs.  Every workgroup reads the whole activation
+// matrix (from L2): four times the weight bytes, which is why the plan
+// keeps it to small weights.
+template <int W>
+__global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
+  constexpr int kR = 3;
+  constexpr int NT = 1;
+  __shared__ f32x4 red[W][NT][kWave];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int ncol = lane & 15, kq = lane >> 4;
+  const int t = blockIdx.x;
+  const int G = a.G;
+  const int g0 = wave * G / W, n = (wave + 1) * G / W - g0;  // >= 1: the plan keeps G >= W
+  const uint32_t q_bytes = (uint32_t)((size_t)a.K * a.N / 2), sz_bytes = (uint32_t)((size_t)a.N * G * 4);
+  const auto rq = buffer_rsrc(a.w0.q, q_bytes), rs = buffer_rsrc(a.w0.sz, sz_bytes);
+  const auto ra = buffer_rsrc(a.a, (uint32_t)(G * 4 * kWave * 16));
+  const uint32_t lane16 = (uint32_t)lane * 16u, col4 = (uint32_t)ncol * 4u;
+  struct Stage {
+    u32x4 b[NT];
+    uint32_t sz[NT];
+    u32x4 x[4];
+  };
+  // group i of this wave's range (loads past its end repeat its last group)
+  auto load = [&](Stage& st, int i) {
+    const int g = g0 + (i < n ? i : n - 1);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const uint32_t tg = (uint32_t)(t * G + g);
+      st.b[nt] = buffer_load_x4(rq, lane16, tg * 1024u);
+      st.sz[nt] = buffer_load_x1(rs, col4, tg * 64u);
+    }
+#pragma unroll
+    for (int f = 0; f < 4; ++f) st.x[f] = buffer_load_x4(ra, lane16, (uint32_t)((g * 4 + f) * 1024));
+  };
+  uint32_t magic_lo = 0x64006400u, magic_hi = 0x54005400u;
+  asm volatile("" : "+v"(magic_lo), "+v"(magic_hi));
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  Stage ring[kR];
+#pragma unroll
+  for (int j = 0; j < kR - 1; ++j) load(ring[j], j);
+  for (int i0 = 0; i0 < n; i0 += kR) {
+#pragma unroll
+    for (int J = 0; J < kR; ++J) {
+      const int i = i0 + J;
+      load(ring[(J + kR - 1) % kR], i + kR - 1);
+      const Stage& st = ring[J];
+      if (i < n) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const BFrag bf = dequant_block(st.b[nt], st.sz[nt], magic_lo, magic_hi);
+          f32x4 cc = {0.f, 0.f, 0.f, 0.f};
+          cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(st.x[0]), bf.lo_a, cc, 0, 0, 0);
+          cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(st.x[1]), bf.lo_b, cc, 0, 0, 0);
+          cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(st.x[2]), bf.hi_a, cc, 0, 0, 0);
+          cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(st.x[3]), bf.hi_b, cc, 0, 0, 0);
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            acc[nt][r] = __builtin_fmaf(cc[r], (float)bitcast<half2v>(st.sz[nt])[0], acc[nt][r]);
+        }
+      } else {
+        // retire the slot's pending loads before the registers are reused
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) asm volatile("" : : "v"(st.b[nt]), "v"(st.sz[nt]));
+#pragma unroll
+        for (int f = 0; f < 4; ++f) asm volatile("" : : "v"(st.x[f]));
+      }
+    }
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) red[wave][nt][lane] = acc[nt];
+  __syncthreads();
+  if (wave != 0) return;
+  f32x4 sum[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    sum[nt] = red[0][nt][lane];
+#pragma unroll
+    for (int w = 1; w < W; ++w) sum[nt] += red[w][nt][lane];
+  }
+  const int col = t * 16 + ncol;
+  const int G2 = a.N >> 7;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int m = 4 * kq + r;
+    if (m < a.M) {
+      const uint16_t h = f2h(sum[0][r] + (a.res ? h2f(a.res[(size_t)m * a.ldr + col]) : 0.f));
+      if (a.y) a.y[(size_t)m * a.ldy + col] = h;
+      if (a.yp) store_prepared(a.yp, m, col, G2, h);
+    }
+  }
+}
+
 // ------------------------------------------------------- activation prep
 // x [M][ldx] fp16 -> prepared layout; one thread per (M-tile, group, lane).
 __global__ __launch_bounds__(256) void prepare_activations_kernel(const uint16_t* __restrict__ x, int M,
@@ -646,7 +766,34 @@ static void launch_mt(const GemmLaunch& L, hipStream_t st) {
   }
 }
 
+template <int W>
+static void launch_kslice(const GemmLaunch& L, hipStream_t st) {
+  GemmArgs a = {};
+  auto unpack = [&](const void* p) {
+    return W4Ptr{reinterpret_cast<const u32x4*>(p),
+                 reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(p) + (size_t)L.K * L.N / 2)};
+  };
+  a.w0 = unpack(L.w0);
+  a.w1 = unpack(L.w1);
+  a.K = L.K;
+  a.N = L.N;
+  a.G = L.K / 128;
+  a.a = L.aprep;
+  a.M = L.M;
+  a.y = L.y;
+  a.ldy = L.ldy;
+  a.yp = L.yprep;
+  a.res = L.res;
+  a.ldr = L.ldr;
+  hipLaunchKernelGGL((w4a16_kslice_kernel<W>), dim3(L.N / 16), dim3(64 * W), 0, st, a);
+}
+
 void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st) {
+  if (L.ksw) {
+    if (L.ksw == 8) launch_kslice<8>(L, st);
+    else launch_kslice<4>(L, st);
+    return;
+  }
   if (L.swiglu) launch_mt<EPI_SWIGLU>(L, st);
   else launch_mt<EPI_PLAIN>(L, st);
 }
@@ -657,6 +804,22 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
   GemmPlan p;
   const int tiles = N / 16;
   const int MT = (M + 15) / 16;
+  const int G = K / 128;
+  if (!swiglu && MT == 1 && G >= 8 && tiles >= 128 && (size_t)K * N / 2 <= ((size_t)16 << 20)) {
+    // up to 16 rows and at most 16 MB of weights: one workgroup per column
+    // tile, K split across its waves, no partials or fix-up (measured: 1B
+    // QKV 8.8 -> 4.2 us, O 8.4 -> 4.4 us, down 10.7 -> 8.8 us; 8B O 10.1 ->
+    // 6.6 us; TP4 shard QKV 11.4 -> 8.9 us, O 10.0 -> 7.1 us; at 29 MB (8B
+    // and shard down projections) a tie, and as a fused SwiGLU slower, the
+    // activation reads from L2 growing with the column count)
+    p.ksw = G >= 16 ? 8 : 4;
+    p.nw = 1;
+    p.nblocks = tiles;
+    p.nwg = tiles;
+    p.part_bytes = 0;
+    p.prep_bytes = (size_t)MT * G * 4 * kWave * 16;
+    return p;
+  }
   if (swiglu && MT <= 2 && tiles % 2 == 0 && tiles / 4 < 256 && tiles / 2 >= 256) {
     // gate and up tiles in different waves, one workgroup per 2 columns:
     // where the 4-column blocks are too few to fill the chip on their own

@@ -194,6 +194,16 @@ def test_w4a16_gemm_small_shapes_ragged_M(M):
     _gemm_case(M, 1024, 320, seed=M, residual=(M % 2 == 0))
 
 
+@pytest.mark.parametrize("M,K,N", [(1, 1024, 2048), (5, 1920, 2048), (8, 2048, 3072), (13, 8192, 2048),
+                                   (16, 4096, 4096), (16, 1152, 4096)])
+def test_w4a16_gemm_k_split_workgroups(M, K, N):
+    """Up to 16 rows and at most 16 MB of weights: one workgroup per
+    column tile, 4 (K < 2048) or 8 waves splitting K into unequal group
+    ranges where G is not a multiple of the wave count (K = 1152, 1920),
+    partials added in wave order; with and without residual, ragged M."""
+    _gemm_case(M, K, N, seed=M * 7 + K, residual=(M % 2 == 1))
+
+
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
 def test_w4a16_gemm_config_shapes(name):
     cfg = CONFIGS[name]

@@ -1023,8 +1023,11 @@ AttnPlan plan_tree_attention(int T, int Hq, int Hkv, int D, int S_max, bool draf
   // about two workgroups per compute unit for the target kernel with up to 4
   // waves (one for the 8-wave target workgroups and for the draft kernel)
   int ns = (draft || VW == 16 ? 256 : 512) / groups - 1;
-  const int max_tiles = (S_max - T + kKeyTile - 1) / kKeyTile;
-  if (ns > max_tiles / 2) ns = max_tiles / 2;
+  // the draft kernel's splits span at least two 64-key tiles; the target
+  // kernel's at least one 32-key stage (the 1B layer, 512 keys and 8 KV
+  // heads: 5 -> 16 parts, attention + merge 10.0 -> 9.2 us)
+  const int max_splits = draft ? (S_max - T + kKeyTile - 1) / kKeyTile / 2 : (S_max - T + kFastKeys - 1) / kFastKeys;
+  if (ns > max_splits) ns = max_splits;
   // at most 16 parts for the draft kernel, and for the target kernel when
   // workgroups of up to 4 waves cover at least 8 row groups (there the merge,
   // which re-reads every part, costs more than the longer splits)

@@ -257,11 +257,14 @@ void w4a16_gemm_kernel(GemmArgs a) {
       st.sz[nt] = buffer_load_x1(up ? rs1 : rs0, col4, tg * 64u);
     }
   };
-  // wave w stages fragment w of every M-tile of the cursor's group
+  // wave w stages fragment w of every M-tile of the cursor's group; with
+  // one M-tile, lanes of rows at or past M load nothing (those rows are
+  // zeros in the prepared layout; whatever the register holds reaches only
+  // output rows that are not written)
   auto load_a = [&](u32x4 (&r)[MT]) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
-      r[mt] = buffer_load_x4(ra, lane16, (uint32_t)(((mt * G + ld_g) * 4 + wave) * 1024));
+      if (MT > 1 || ncol < a.M) r[mt] = buffer_load_x4(ra, lane16, (uint32_t)(((mt * G + ld_g) * 4 + wave) * 1024));
   };
   auto store_a = [&](int slot, const u32x4 (&r)[MT]) {
 #pragma unroll
@@ -567,8 +570,12 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
       st.b[nt] = buffer_load_x4(rq, lane16, tg * 1024u);
       st.sz[nt] = buffer_load_x1(rs, col4, tg * 64u);
     }
+    // lanes of rows at or past M load nothing (zeros in the prepared
+    // layout; the MFMA rows they feed are not written)
+    if (ncol < a.M) {
 #pragma unroll
-    for (int f = 0; f < 4; ++f) st.x[f] = buffer_load_x4(ra, lane16, (uint32_t)((g * 4 + f) * 1024));
+      for (int f = 0; f < 4; ++f) st.x[f] = buffer_load_x4(ra, lane16, (uint32_t)((g * 4 + f) * 1024));
+    }
   };
   uint32_t magic_lo = 0x64006400u, magic_hi = 0x54005400u;
   asm volatile("" : "+v"(magic_lo), "+v"(magic_hi));

@@ -541,10 +541,10 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
 // and no second kernel runs.  Every workgroup reads the whole activation
 // matrix (from L2): four times the weight bytes, which is why the plan
 // keeps it to small weights.
-template <int W>
+template <int W, int NT>
 __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   constexpr int kR = 3;
-  constexpr int NT = 1;
+  static_assert(NT == 1 || NT == 2, "plain, or fused SwiGLU (gate and up tile of one column tile)");
   __shared__ f32x4 red[W][NT][kWave];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -553,7 +553,9 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   const int G = a.G;
   const int g0 = wave * G / W, n = (wave + 1) * G / W - g0;  // >= 1: the plan keeps G >= W
   const uint32_t q_bytes = (uint32_t)((size_t)a.K * a.N / 2), sz_bytes = (uint32_t)((size_t)a.N * G * 4);
-  const auto rq = buffer_rsrc(a.w0.q, q_bytes), rs = buffer_rsrc(a.w0.sz, sz_bytes);
+  const auto rq0 = buffer_rsrc(a.w0.q, q_bytes), rs0 = buffer_rsrc(a.w0.sz, sz_bytes);
+  const auto rq1 = buffer_rsrc(NT == 2 ? a.w1.q : a.w0.q, q_bytes);
+  const auto rs1 = buffer_rsrc(NT == 2 ? a.w1.sz : a.w0.sz, sz_bytes);
   const auto ra = buffer_rsrc(a.a, (uint32_t)(G * 4 * kWave * 16));
   const uint32_t lane16 = (uint32_t)lane * 16u, col4 = (uint32_t)ncol * 4u;
   struct Stage {
@@ -567,8 +569,8 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const uint32_t tg = (uint32_t)(t * G + g);
-      st.b[nt] = buffer_load_x4(rq, lane16, tg * 1024u);
-      st.sz[nt] = buffer_load_x1(rs, col4, tg * 64u);
+      st.b[nt] = buffer_load_x4(nt ? rq1 : rq0, lane16, tg * 1024u);
+      st.sz[nt] = buffer_load_x1(nt ? rs1 : rs0, col4, tg * 64u);
     }
     // lanes of rows at or past M load nothing (zeros in the prepared
     // layout; the MFMA rows they feed are not written)
@@ -630,7 +632,14 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   for (int r = 0; r < 4; ++r) {
     const int m = 4 * kq + r;
     if (m < a.M) {
-      const uint16_t h = f2h(sum[0][r] + (a.res ? h2f(a.res[(size_t)m * a.ldr + col]) : 0.f));
+      float val;
+      if constexpr (NT == 2) {
+        const float gte = sum[0][r];
+        val = gte / (1.0f + __expf(-gte)) * sum[1][r];
+      } else {
+        val = sum[0][r] + (a.res ? h2f(a.res[(size_t)m * a.ldr + col]) : 0.f);
+      }
+      const uint16_t h = f2h(val);
       if (a.y) a.y[(size_t)m * a.ldy + col] = h;
       if (a.yp) store_prepared(a.yp, m, col, G2, h);
     }
@@ -773,7 +782,7 @@ static void launch_mt(const GemmLaunch& L, hipStream_t st) {
   }
 }
 
-template <int W>
+template <int W, int NT>
 static void launch_kslice(const GemmLaunch& L, hipStream_t st) {
   GemmArgs a = {};
   auto unpack = [&](const void* p) {
@@ -792,13 +801,18 @@ static void launch_kslice(const GemmLaunch& L, hipStream_t st) {
   a.yp = L.yprep;
   a.res = L.res;
   a.ldr = L.ldr;
-  hipLaunchKernelGGL((w4a16_kslice_kernel<W>), dim3(L.N / 16), dim3(64 * W), 0, st, a);
+  hipLaunchKernelGGL((w4a16_kslice_kernel<W, NT>), dim3(L.N / 16), dim3(64 * W), 0, st, a);
 }
 
 void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st) {
   if (L.ksw) {
-    if (L.ksw == 8) launch_kslice<8>(L, st);
-    else launch_kslice<4>(L, st);
+    if (L.swiglu) {
+      if (L.ksw == 8) launch_kslice<8, 2>(L, st);
+      else launch_kslice<4, 2>(L, st);
+    } else {
+      if (L.ksw == 8) launch_kslice<8, 1>(L, st);
+      else launch_kslice<4, 1>(L, st);
+    }
     return;
   }
   if (L.swiglu) launch_mt<EPI_SWIGLU>(L, st);
@@ -812,14 +826,20 @@ GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu) {
   const int tiles = N / 16;
   const int MT = (M + 15) / 16;
   const int G = K / 128;
-  if (!swiglu && MT == 1 && G >= 8 && tiles >= 128 && (size_t)K * N / 2 <= ((size_t)16 << 20)) {
-    // up to 16 rows and at most 16 MB of weights: one workgroup per column
-    // tile, K split across its waves, no partials or fix-up (measured: 1B
-    // QKV 8.8 -> 4.2 us, O 8.4 -> 4.4 us, down 10.7 -> 8.8 us; 8B O 10.1 ->
-    // 6.6 us; TP4 shard QKV 11.4 -> 8.9 us, O 10.0 -> 7.1 us; at 29 MB (8B
-    // and shard down projections) a tie, and as a fused SwiGLU slower, the
-    // activation reads from L2 growing with the column count)
-    p.ksw = G >= 16 ? 8 : 4;
+  const size_t mbytes = (size_t)K * N / 2;
+  if (MT == 1 && G >= 8 && tiles >= 128 && mbytes <= ((size_t)32 << 20) && (!swiglu || M <= 8)) {
+    // up to 16 rows (a fused SwiGLU: up to 8) and at most 32 MB per matrix:
+    // one workgroup per column tile, K split across its waves, no partials
+    // or fix-up.  Every workgroup reads the activations of the rows it
+    // computes (rows past M are not loaded), so the L2 reads are M / 4
+    // (SwiGLU: M / 8) times the weight bytes.  Measured against the forms below:
+    // 1B QKV 8.8 -> 4.2 us, O 8.4 -> 4.4 us, down 10.7 -> 7.0 us, SwiGLU
+    // 9.5 -> 7.4 us; 8B O 10.1 -> 6.6 us, down 15.4 -> 14.5 us; TP4 shard
+    // QKV 11.4 -> 8.9 us, O 10.0 -> 7.1 us, SwiGLU 20.5 -> 16.2 us, down
+    // 15.4 -> 13.4 us.  The 8B SwiGLU at 16 rows (twice the activation
+    // reads) is slower, 17.5 -> 21.4 us, and stays on the 2-column form.
+    // A SwiGLU workgroup streams two tiles: 4 waves (8: 7.4 -> 8.5 us).
+    p.ksw = (!swiglu && G >= 16) ? 8 : 4;
     p.nw = 1;
     p.nblocks = tiles;
     p.nwg = tiles;

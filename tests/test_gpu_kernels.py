@@ -197,10 +197,11 @@ def test_w4a16_gemm_small_shapes_ragged_M(M):
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 2048), (5, 1920, 2048), (8, 2048, 3072), (13, 8192, 2048),
                                    (16, 4096, 4096), (16, 1152, 4096)])
 def test_w4a16_gemm_k_split_workgroups(M, K, N):
-    """Up to 16 rows and at most 16 MB of weights: one workgroup per
-    column tile, 4 (K < 2048) or 8 waves splitting K into unequal group
-    ranges where G is not a multiple of the wave count (K = 1152, 1920),
-    partials added in wave order; with and without residual, ragged M."""
+    """Up to 16 rows and at most 32 MB of weights (the 8B down projection,
+    29 MB, runs in the config-shape test): one workgroup per column tile, 4
+    (K < 2048) or 8 waves splitting K into unequal group ranges where G is
+    not a multiple of the wave count (K = 1152, 1920), partials added in wave
+    order; with and without residual, ragged M."""
     _gemm_case(M, K, N, seed=M * 7 + K, residual=(M % 2 == 1))
 
 
@@ -308,14 +309,10 @@ def test_w4a16_swiglu_70b_width(M):
     check_close(y[:, cols], ref, f"swiglu 70b width M={M}")
 
 
-@pytest.mark.parametrize("M,K,N", [(16, 4096, 14336), (1, 4096, 14336), (17, 4096, 14336), (32, 4096, 14336),
-                                   (8, 2048, 8192), (31, 2048, 8192)])
-def test_w4a16_swiglu_two_column_blocks(M, K, N):
-    """SwiGLU at the 8B and 1B FFN widths, where the gate and up tiles of a
-    column run in different waves of one workgroup: sampled columns (the first
-    and last 64, 256 random ones) against the oracle, and two calls agree bit
-    for bit."""
-    Wg, Wu = _rand_w4(31 + M, N, K), _rand_w4(32 + M, N, K)
+def _swiglu_sampled_case(M, K, N, seed):
+    """Two calls agree bit for bit; sampled columns (the first and last 64,
+    256 random ones) against the oracle."""
+    Wg, Wu = _rand_w4(seed, N, K), _rand_w4(seed + 1, N, K)
     x = gen.normal_f16(33, M, (M, K))
     tg, dg = upload_w4(Wg)
     tu, du = upload_w4(Wu)
@@ -331,6 +328,26 @@ def test_w4a16_swiglu_two_column_blocks(M, K, N):
                            np.random.default_rng(34).choice(np.arange(64, N - 64), 256, replace=False)])
     ref = oracle.w4a16_swiglu(_w4_rows(Wg, cols), _w4_rows(Wu, cols), x)
     check_close(outs[0][:, cols], ref, f"swiglu M={M} K={K} N={N}")
+
+
+@pytest.mark.parametrize("M,K,N", [(1, 4096, 14336), (8, 2048, 8192), (5, 8192, 7168), (8, 1152, 2048),
+                                   (3, 1920, 4096)])
+def test_w4a16_swiglu_k_split_workgroups(M, K, N):
+    """Fused SwiGLU at up to 8 rows and at most 32 MB per matrix (the 1B FFN,
+    the 8B FFN at one row, one GPU's share of the 70B FFN under 4-way tensor
+    parallelism): one workgroup per column tile reads its gate and up tiles,
+    4 waves split K (unequal group ranges at K = 1152 and 1920)."""
+    _swiglu_sampled_case(M, K, N, seed=41 + M)
+
+
+@pytest.mark.parametrize("M,K,N", [(16, 4096, 14336), (9, 4096, 14336), (17, 4096, 14336), (32, 4096, 14336),
+                                   (9, 2048, 8192), (31, 2048, 8192)])
+def test_w4a16_swiglu_two_column_blocks(M, K, N):
+    """SwiGLU at the 8B and 1B FFN widths above 8 rows, where the gate and
+    up tiles of a column run in different waves of one workgroup: sampled
+    columns (the first and last 64, 256 random ones) against the oracle, and
+    two calls agree bit for bit."""
+    _swiglu_sampled_case(M, K, N, seed=31 + M)
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 1024), (8, 2048, 512), (13, 1024, 2048), (32, 8192, 1024),

@@ -165,6 +165,29 @@ int swiftspec_w4a16_swiglu_prepared(const swiftspec_w4* Wg, const swiftspec_w4* 
 int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, const uint16_t* gamma,
                       float eps, uint16_t* out, int32_t ldo, void* stream);
 
+/* RMSNorm followed by a projection: the QKV projection of the attention
+ * block and the fused SwiGLU of the MLP block read the normalised residual
+ * stream (Sec. 2's decoder layer):
+ *   swiftspec_rmsnorm_w4a16_gemm  : y = fp16( xn . W'^T )
+ *   swiftspec_rmsnorm_w4a16_swiglu: y = fp16( silu(xn . Wg'^T) * (xn . Wu'^T) )
+ * with xn[m] = x[m] / sqrt(mean_k x[m][k]^2 + eps) * gamma over the K
+ * columns.  Where the GEMM's plan gives each workgroup all of K (up to 16
+ * rows, SwiGLU up to 8; K <= 8192; matrices of at most 32 MB) the norm
+ * runs inside it:
+ * the matrix-core operand is fp16(x * gamma) and row m of the fp32 product
+ * is scaled by 1 / sqrt(mean x[m]^2 + eps) before the epilogue; otherwise
+ * xn is formed in fp16 (as swiftspec_rmsnorm) and multiplied.  Both are
+ * within the GEMM tolerance of the fp64 definition.  x [M][ldx], gamma [K]
+ * fp16, 16-byte aligned, ldx % 8 == 0; no residual; the workspace of
+ * swiftspec_w4a16_gemm_workspace_bytes / _swiglu_workspace_bytes.  Other
+ * arguments and errors as swiftspec_w4a16_gemm / _swiglu. */
+int swiftspec_rmsnorm_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, int32_t ldx,
+                                 const uint16_t* gamma, float eps, uint16_t* y, int32_t ldy, void* ws,
+                                 size_t ws_bytes, void* stream);
+int swiftspec_rmsnorm_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* x,
+                                   int32_t M, int32_t ldx, const uint16_t* gamma, float eps, uint16_t* y,
+                                   int32_t ldy, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------- tree attention
  * Tree-masked grouped-query attention of the T draft tokens over the KV
  * cache (Sec. 3.1 target-side square mask; Sec. 3.3 masked attention with
@@ -441,8 +464,12 @@ typedef struct {
  *   xn = rmsnorm(x, attn_norm); qkv = xn.Wqkv'^T; o = tree_attention(qkv)
  *   h = x + o.Wo'^T; hn = rmsnorm(h, mlp_norm); m = silu(hn.Wg'^T) * (hn.Wu'^T)
  *   out = h + m.Wd'^T
- * with fp16 storage of xn, qkv, o, h, hn, m, out.  hidden [T][H] is read as
- * x and overwritten with out.  The caches receive the tree's keys and values
+ * with fp16 storage of qkv, o, h, m, out; the norms run with the
+ * projections that read them (swiftspec_rmsnorm_w4a16_gemm / _swiglu), so
+ * xn and hn are stored only where those form them in fp16.  The layer is
+ * exactly the composition rmsnorm_w4a16_gemm, tree_attention, w4a16_gemm
+ * (+ residual), rmsnorm_w4a16_swiglu, w4a16_gemm (+ residual).  hidden
+ * [T][H] is read as x and overwritten with out.  The caches receive the tree's keys and values
  * at rows [P, P+T).  softmax scale 1/sqrt(D). */
 int swiftspec_verify_layer(const swiftspec_layer* layer, const swiftspec_dims* dims,
                            uint16_t* hidden, int32_t T, const int32_t* d_prefix_len,
@@ -450,8 +477,8 @@ int swiftspec_verify_layer(const swiftspec_layer* layer, const swiftspec_dims* d
                            size_t ws_bytes, void* stream);
 size_t swiftspec_verify_layer_workspace_bytes(const swiftspec_dims* dims, int32_t T);
 /* Byte offsets, inside the verify_layer workspace, of the layer's fp16
- * intermediates after a call: offsets[0..5] = xn [T][H], qkv [T][(Hq+2Hkv)D],
- * o [T][Hq D], h [T][H], hn [T][H], m [T][F] (row-major, dense).  For
+ * intermediates after a call: offsets[0..3] = qkv [T][(Hq+2Hkv)D],
+ * o [T][Hq D], h [T][H], m [T][F] (row-major, dense).  For
  * inspection and stage-by-stage checking; the contents are valid until the
  * next call that uses the workspace. */
 int swiftspec_verify_layer_workspace_layout(const swiftspec_dims* dims, int32_t T, size_t* offsets);

@@ -91,6 +91,10 @@ _SIGS = {
     "swiftspec_w4a16_swiglu_prepared": ([ctypes.POINTER(W4), ctypes.POINTER(W4), vp, i32, vp, i32, vp, sz, vp],
                                         ctypes.c_int),
     "swiftspec_rmsnorm": ([vp, i32, i32, i32, vp, f32, vp, i32, vp], ctypes.c_int),
+    "swiftspec_rmsnorm_w4a16_gemm": ([ctypes.POINTER(W4), vp, i32, i32, vp, f32, vp, i32, vp, sz, vp],
+                                     ctypes.c_int),
+    "swiftspec_rmsnorm_w4a16_swiglu": ([ctypes.POINTER(W4), ctypes.POINTER(W4), vp, i32, i32, vp, f32, vp, i32,
+                                       vp, sz, vp], ctypes.c_int),
     "swiftspec_tree_attention": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, f32,
                                   vp, i32, vp, sz, vp], ctypes.c_int),
     "swiftspec_tree_attention_workspace_bytes": ([i32, i32, i32, i32, i32], sz),
@@ -300,6 +304,22 @@ def rmsnorm(x, gamma, out, eps=1e-5, stream=None):
     st = _load().swiftspec_rmsnorm(_ptr(x), x.shape[0], x.shape[1], x.stride(0), _ptr(gamma), eps,
                                    _ptr(out), out.stride(0), _stream(stream))
     _check(st, "rmsnorm")
+
+
+def rmsnorm_w4a16_gemm(W: W4, x, gamma, y, ws, eps=1e-5, stream=None):
+    """y = rmsnorm(x, gamma) . W'^T (workspace of gemm_workspace_bytes)."""
+    st = _load().swiftspec_rmsnorm_w4a16_gemm(ctypes.byref(W), _ptr(x), x.shape[0], x.stride(0), _ptr(gamma), eps,
+                                              _ptr(y), y.stride(0), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "rmsnorm_w4a16_gemm")
+
+
+def rmsnorm_w4a16_swiglu(Wg: W4, Wu: W4, x, gamma, y, ws, eps=1e-5, stream=None):
+    """y = silu(xn . Wg'^T) * (xn . Wu'^T), xn = rmsnorm(x, gamma)
+    (workspace of swiglu_workspace_bytes)."""
+    st = _load().swiftspec_rmsnorm_w4a16_swiglu(ctypes.byref(Wg), ctypes.byref(Wu), _ptr(x), x.shape[0],
+                                                x.stride(0), _ptr(gamma), eps, _ptr(y), y.stride(0), _ptr(ws),
+                                                ws.numel(), _stream(stream))
+    _check(st, "rmsnorm_w4a16_swiglu")
 
 
 def tree_attention_workspace_bytes(T, Hq, Hkv, D, S_max) -> int:
@@ -524,15 +544,15 @@ def verify_layer_workspace_bytes(dims: Dims, T: int) -> int:
 
 
 def verify_layer_intermediates(dims: Dims, T: int, ws):
-    """Views (int16 bits) of the layer intermediates xn, qkv, o, h, hn, m
-    held in a verify_layer workspace."""
-    offs = (sz * 6)()
+    """Views (int16 bits) of the layer intermediates qkv, o, h, m held in a
+    verify_layer workspace."""
+    offs = (sz * 4)()
     _check(_load().swiftspec_verify_layer_workspace_layout(ctypes.byref(dims), T, offs),
            "verify_layer_workspace_layout")
     import torch
     n_qkv = (dims.Hq + 2 * dims.Hkv) * dims.D
-    cols = [dims.H, n_qkv, dims.Hq * dims.D, dims.H, dims.H, dims.F]
-    names = ["xn", "qkv", "o", "h", "hn", "m"]
+    cols = [n_qkv, dims.Hq * dims.D, dims.H, dims.F]
+    names = ["qkv", "o", "h", "m"]
     out = {}
     for name, off, c in zip(names, offs, cols):
         out[name] = ws[off:off + T * c * 2].view(torch.int16).view(T, c)

@@ -68,7 +68,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (_Float16)(((float)h[e] * inv) * (float)gm[e]);
       const u32x4 ob = bitcast<u32x4>(o);
-      *reinterpret_cast<u32x4*>(orow + 32 * c + 8 * q) = ob;
+      if (out) *reinterpret_cast<u32x4*>(orow + 32 * c + 8 * q) = ob;
 #pragma unroll
       for (int e = 0; e < 4; ++e) w[4 * q + e] = ob[e];
     }

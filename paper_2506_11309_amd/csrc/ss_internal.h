@@ -14,6 +14,12 @@ struct GemmLaunch {
   int K, N;       // N = output columns
   const uint16_t* aprep;  // activations in the prepared layout
   int M;
+  // non-null (K-split plans only, ksw > 0): the input is RMSNorm(xnorm)
+  // with weight gamma [K], computed in the GEMM; aprep is not read
+  const uint16_t* xnorm = nullptr;
+  int ldx = 0;
+  const uint16_t* gamma = nullptr;
+  float eps = 0.f;
   uint16_t* y;      // plain output (nullable)
   int ldy;
   uint16_t* yprep;  // prepared output for a following GEMM (nullable)
@@ -26,6 +32,9 @@ struct GemmLaunch {
   bool swiglu;
   float* part;  // split-K partial slots (2 per workgroup)
 };
+
+// Widest K whose RMSNorm a K-split GEMM applies itself (gamma staged in LDS).
+constexpr int kNormMaxK = 8192;
 
 struct GemmPlan {
   int nw, nblocks, nwg, ksw = 0;

@@ -68,12 +68,31 @@ size_t gemm_ws(int M, int K, int N, bool swiglu) {
 }
 
 // Launch a validated W4A16 GEMM / SwiGLU reading prepared activations.
+// With `norm` (x, ldx, gamma, eps) the input is RMSNorm(x), computed inside
+// the GEMM; only K-split plans take it (norm_in_gemm).
+struct NormIn {
+  const uint16_t* x;
+  int ldx;
+  const uint16_t* gamma;
+  float eps;
+};
+
+bool norm_in_gemm(int M, const swiftspec_w4* W0, bool swiglu) {
+  return W0->K <= ss::kNormMaxK && ss::plan_w4a16_gemm(M, W0->K, W0->N, swiglu).ksw > 0;
+}
+
 void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* aprep, int M,
               uint16_t* y, int ldy, uint16_t* yprep, const uint16_t* res, int ldr, void* ws,
-              float* part, hipStream_t st) {
+              float* part, hipStream_t st, const NormIn* norm = nullptr) {
   const bool swiglu = W1 != nullptr;
   ss::GemmPlan p = ss::plan_w4a16_gemm(M, W0->K, W0->N, swiglu);
   ss::GemmLaunch L;
+  if (norm) {
+    L.xnorm = norm->x;
+    L.ldx = norm->ldx;
+    L.gamma = norm->gamma;
+    L.eps = norm->eps;
+  }
   L.w0 = W0->packed;
   L.w1 = swiglu ? W1->packed : W0->packed;
   L.K = W0->K;
@@ -92,6 +111,19 @@ void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* ap
   L.swiglu = swiglu;
   L.part = part;
   ss::launch_w4a16_gemm(L, st);
+}
+
+// RMSNorm(x; gamma, eps) followed by the GEMM / SwiGLU: inside the GEMM
+// where its plan splits K within workgroups, else the norm kernel writes
+// the prepared operand into xprep and the GEMM reads it.
+void run_norm_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const NormIn& n, int M, uint16_t* y,
+                   int ldy, uint16_t* yprep, uint16_t* xprep, void* ws, float* part, hipStream_t st) {
+  if (norm_in_gemm(M, W0, W1 != nullptr)) {
+    run_gemm(W0, W1, nullptr, M, y, ldy, yprep, nullptr, 0, ws, part, st, &n);
+  } else {
+    ss::launch_rmsnorm(n.x, M, W0->K, n.ldx, n.gamma, n.eps, nullptr, 0, xprep, st);
+    run_gemm(W0, W1, xprep, M, y, ldy, yprep, nullptr, 0, ws, part, st);
+  }
 }
 
 // Standalone entry: prepare plain x into the workspace, then run the GEMM.
@@ -199,7 +231,7 @@ void* noalloc_scratch(int* rc) {
 }
 
 struct LayerWs {
-  size_t xn, qkv, o, h, hn, m, xn_p, o_p, hn_p, m_p, part, total;
+  size_t qkv, o, h, m, xn_p, o_p, hn_p, m_p, part, total;
 };
 
 LayerWs layer_ws(const swiftspec_dims* d, int T) {
@@ -212,11 +244,9 @@ LayerWs layer_ws(const swiftspec_dims* d, int T) {
     off += align_up(bytes);
     return o;
   };
-  w.xn = take((size_t)T * d->H * 2);
   w.qkv = take((size_t)T * Nqkv * 2);
   w.o = take((size_t)T * d->Hq * d->D * 2);
   w.h = take((size_t)T * d->H * 2);
-  w.hn = take((size_t)T * d->H * 2);
   w.m = take((size_t)T * d->F * 2);
   w.xn_p = take(MT16 * d->H * 2);
   w.o_p = take(MT16 * d->Hq * d->D * 2);
@@ -365,6 +395,53 @@ int swiftspec_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const
   if (M == 0) return SWIFTSPEC_OK;
   if (ws_bytes < gemm_ws(M, Wg->K, Wg->N, true)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
   run_gemm_plain(Wg, Wu, x, M, ldx, y, ldy, nullptr, 0, ws, S(stream));
+  return check_launch();
+}
+
+// Argument checks shared by the RMSNorm + GEMM / SwiGLU entry points.
+static int check_norm_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* x, int32_t M,
+                           int32_t ldx, const uint16_t* gamma, const uint16_t* y, int32_t ldy, const void* ws) {
+  int rc = check_w4(W0);
+  if (rc) return rc;
+  if (W1) {
+    if ((rc = check_w4(W1))) return rc;
+    if (W0->K != W1->K || W0->N != W1->N) return SWIFTSPEC_INVALID_ARG;
+  }
+  if (!x || !gamma || !y || !ws) return SWIFTSPEC_INVALID_ARG;
+  if (M < 0 || ldx < W0->K || ldy < W0->N) return SWIFTSPEC_INVALID_ARG;
+  if (M > SWIFTSPEC_MAX_M) return SWIFTSPEC_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(gamma) || ldx % 8) return SWIFTSPEC_MISALIGNED;
+  return SWIFTSPEC_OK;
+}
+
+int swiftspec_rmsnorm_w4a16_gemm(const swiftspec_w4* W, const uint16_t* x, int32_t M, int32_t ldx,
+                                 const uint16_t* gamma, float eps, uint16_t* y, int32_t ldy, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  int rc = check_norm_gemm(W, nullptr, x, M, ldx, gamma, y, ldy, ws);
+  if (rc) return rc;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (ws_bytes < gemm_ws(M, W->K, W->N, false)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  const ss::GemmPlan p = ss::plan_w4a16_gemm(M, W->K, W->N, false);
+  char* base = static_cast<char*>(ws);
+  run_norm_gemm(W, nullptr, NormIn{x, ldx, gamma, eps}, M, y, ldy, nullptr,
+                reinterpret_cast<uint16_t*>(base + kHeader),
+                ws, reinterpret_cast<float*>(base + kHeader + align_up(p.prep_bytes)), S(stream));
+  return check_launch();
+}
+
+int swiftspec_rmsnorm_w4a16_swiglu(const swiftspec_w4* Wg, const swiftspec_w4* Wu, const uint16_t* x,
+                                   int32_t M, int32_t ldx, const uint16_t* gamma, float eps, uint16_t* y,
+                                   int32_t ldy, void* ws, size_t ws_bytes, void* stream) {
+  if (!Wu) return SWIFTSPEC_INVALID_ARG;
+  int rc = check_norm_gemm(Wg, Wu, x, M, ldx, gamma, y, ldy, ws);
+  if (rc) return rc;
+  if (M == 0) return SWIFTSPEC_OK;
+  if (ws_bytes < gemm_ws(M, Wg->K, Wg->N, true)) return SWIFTSPEC_WORKSPACE_TOO_SMALL;
+  const ss::GemmPlan p = ss::plan_w4a16_gemm(M, Wg->K, Wg->N, true);
+  char* base = static_cast<char*>(ws);
+  run_norm_gemm(Wg, Wu, NormIn{x, ldx, gamma, eps}, M, y, ldy, nullptr,
+                reinterpret_cast<uint16_t*>(base + kHeader),
+                ws, reinterpret_cast<float*>(base + kHeader + align_up(p.prep_bytes)), S(stream));
   return check_launch();
 }
 
@@ -613,12 +690,10 @@ size_t swiftspec_verify_layer_workspace_bytes(const swiftspec_dims* dims, int32_
 int swiftspec_verify_layer_workspace_layout(const swiftspec_dims* dims, int32_t T, size_t* offsets) {
   if (!dims || !offsets || T < 1 || T > SWIFTSPEC_MAX_TREE) return SWIFTSPEC_INVALID_ARG;
   const LayerWs w = layer_ws(dims, T);
-  offsets[0] = w.xn;
-  offsets[1] = w.qkv;
-  offsets[2] = w.o;
-  offsets[3] = w.h;
-  offsets[4] = w.hn;
-  offsets[5] = w.m;
+  offsets[0] = w.qkv;
+  offsets[1] = w.o;
+  offsets[2] = w.h;
+  offsets[3] = w.m;
   return SWIFTSPEC_OK;
 }
 
@@ -651,17 +726,18 @@ static void enqueue_layer(const swiftspec_layer* Lw, const swiftspec_dims* d, ui
   const LayerWs w = layer_ws(d, T);
   char* base = static_cast<char*>(ws);
   auto at = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
-  uint16_t *xn = at(w.xn), *qkv = at(w.qkv), *o = at(w.o), *h = at(w.h), *hn = at(w.hn), *m = at(w.m);
+  uint16_t *qkv = at(w.qkv), *o = at(w.o), *h = at(w.h), *m = at(w.m);
   uint16_t *xn_p = at(w.xn_p), *o_p = at(w.o_p), *hn_p = at(w.hn_p), *m_p = at(w.m_p);
   float* part = reinterpret_cast<float*>(base + w.part);
-  ss::launch_rmsnorm(hidden, T, H, H, Lw->attn_norm, d->eps, xn, H, xn_p, st);
-  run_gemm(&Lw->wqkv, nullptr, xn_p, T, qkv, Nqkv, nullptr, nullptr, 0, ws, part, st);
+  // the RMSNorms in front of the QKV and the FFN projections run with them
+  // (swiftspec_rmsnorm_w4a16_gemm / _swiglu)
+  const NormIn n_attn{hidden, H, Lw->attn_norm, d->eps}, n_mlp{h, H, Lw->mlp_norm, d->eps};
+  run_norm_gemm(&Lw->wqkv, nullptr, n_attn, T, qkv, Nqkv, nullptr, xn_p, ws, part, st);
   run_attention(qkv, Nqkv, qkv + Hd, qkv + Hd + d->Hkv * d->D, Nqkv, Lw->k_cache, Lw->v_cache,
                 d->S_max, d_prefix_len, d_parent, T, d->Hq, d->Hkv, d->D, rope,
                 1.0f / std::sqrt((float)d->D), o, Hd, o_p, ws, part, st);
   run_gemm(&Lw->wo, nullptr, o_p, T, h, H, nullptr, hidden, H, ws, part, st);
-  ss::launch_rmsnorm(h, T, H, H, Lw->mlp_norm, d->eps, hn, H, hn_p, st);
-  run_gemm(&Lw->wgate, &Lw->wup, hn_p, T, m, F, m_p, nullptr, 0, ws, part, st);
+  run_norm_gemm(&Lw->wgate, &Lw->wup, n_mlp, T, m, F, m_p, hn_p, ws, part, st);
   run_gemm(&Lw->wdown, nullptr, m_p, T, hidden, H, nullptr, h, H, ws, part, st);
 }
 

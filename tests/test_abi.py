@@ -80,6 +80,23 @@ def test_host_side_validation_rejects_before_launch(ss):
     assert lib.swiftspec_graph_begin(None) == ss.INVALID_ARG
     # RMSNorm rows: whole 32-element chunks
     assert lib.swiftspec_rmsnorm(fake, 4, 72, 72, fake, ctypes.c_float(1e-5), fake, 72, None) == ss.UNSUPPORTED
+    # RMSNorm + projection: null gamma / up matrix, misaligned gamma, short
+    # leading dimension, too many rows, mismatched SwiGLU pair, workspace
+    eps = ctypes.c_float(1e-5)
+    ng = lambda gam=fake, M=8, ldx=4096, wsb=1 << 30: lib.swiftspec_rmsnorm_w4a16_gemm(
+        ctypes.byref(W), fake, M, ldx, gam, eps, fake, 1024, fake, wsb, None)
+    assert ng(gam=None) == ss.INVALID_ARG
+    assert ng(gam=fake + 2) == ss.MISALIGNED
+    assert ng(ldx=4088) == ss.INVALID_ARG
+    assert ng(M=65) == ss.UNSUPPORTED
+    assert ng(wsb=16) == ss.WORKSPACE_TOO_SMALL
+    W_other = ss.W4(fake, fake, fake, 4096, 2048, fake)
+    assert lib.swiftspec_rmsnorm_w4a16_swiglu(ctypes.byref(W), None, fake, 8, 4096, fake, eps, fake, 1024, fake,
+                                              1 << 30, None) == ss.INVALID_ARG
+    assert lib.swiftspec_rmsnorm_w4a16_swiglu(ctypes.byref(W), ctypes.byref(W_other), fake, 8, 4096, fake, eps,
+                                              fake, 2048, fake, 1 << 30, None) == ss.INVALID_ARG
+    assert lib.swiftspec_rmsnorm_w4a16_swiglu(ctypes.byref(W), ctypes.byref(W), fake, 8, 4096, fake, eps, fake,
+                                              1024, fake, 16, None) == ss.WORKSPACE_TOO_SMALL
     # greedy acceptance: sizes, leading dimension, workspace, null outputs
     acc = lambda T, V, ldl, lg=fake, ws=fake, wsb=1 << 20, bonus=fake: lib.swiftspec_greedy_accept(
         lg, ldl, T, V, fake, fake, fake, fake, bonus, None, ws, wsb, None)

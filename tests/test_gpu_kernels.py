@@ -350,6 +350,51 @@ def test_w4a16_swiglu_two_column_blocks(M, K, N):
     _swiglu_sampled_case(M, K, N, seed=31 + M)
 
 
+@pytest.mark.parametrize("M,K,N,ldx,swiglu", [
+    (8, 2048, 3072, 2048, False), (1, 2048, 3072, 2048, False), (7, 8192, 2560, 8192, False),
+    (8, 1152, 2048, 1280, False), (5, 1920, 2048, 1920, False), (13, 4096, 6144, 4096, False),
+    (16, 1152, 2048, 1288, False), (16, 4096, 4096, 4096, False),  # norm inside the K-split GEMM
+    (3, 16384, 2048, 16384, False),                                # K past the in-GEMM limit
+    (17, 2048, 3072, 2048, False), (32, 8192, 1024, 8200, False),  # norm kernel, then stream-K
+    (8, 2048, 8192, 2048, True), (3, 1920, 4096, 2056, True),      # inside the K-split SwiGLU
+    (9, 2048, 8192, 2048, True)])                                  # norm kernel, then the SwiGLU
+def test_rmsnorm_then_projection_matches_oracle(M, K, N, ldx, swiglu):
+    """RMSNorm followed by the QKV-style projection or the fused SwiGLU,
+    against the reference's fp16 rmsnorm then its fp64 product: where each
+    workgroup holds all of K the norm runs inside the GEMM (operand x *
+    gamma, row scale after the contraction, each row's 16-byte chunks
+    loaded in a row-dependent order), else as its own kernel; both within
+    the GEMM tolerance, with strided rows (ldx > K, also not a multiple of
+    16 bytes apart), ragged M and unequal K ranges per wave (K = 1152,
+    1920); two calls agree bit for bit."""
+    seed = 50 + M + K % 1000
+    x = gen.normal_f16(seed, 0, (M, ldx), 0.0, 2.0)
+    gamma = gen.normal_f16(seed, 1, (K,), 1.0, 0.2)
+    W = _rand_w4(seed + 1, N, K)
+    t, d = upload_w4(W)
+    xn = oracle.rmsnorm(np.ascontiguousarray(x[:, :K]), gamma)
+    if swiglu:
+        Wu = _rand_w4(seed + 2, N, K)
+        tu, du = upload_w4(Wu)
+        ws = ss.workspace(ss.swiglu_workspace_bytes(M, K, N), dev())
+        ref = oracle.w4a16_swiglu(W, Wu, xn)
+    else:
+        ws = ss.workspace(ss.gemm_workspace_bytes(M, K, N), dev())
+        ref = oracle.w4a16_gemm(W, xn)
+    dx, dg = up(x), up(gamma)
+    outs = []
+    for _ in range(2):
+        dy = torch.zeros((M, N), dtype=torch.int16, device=dev())
+        if swiglu:
+            ss.rmsnorm_w4a16_swiglu(d, du, dx, dg, dy, ws)
+        else:
+            ss.rmsnorm_w4a16_gemm(d, dx, dg, dy, ws)
+        torch.cuda.synchronize()
+        outs.append(down16(dy))
+    assert np.array_equal(outs[0], outs[1])
+    check_close(outs[0], ref, f"rmsnorm then {'swiglu' if swiglu else 'gemm'} M={M} K={K} N={N}")
+
+
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 1024), (8, 2048, 512), (13, 1024, 2048), (32, 8192, 1024),
                                    (40, 4096, 1024), (64, 2048, 1024)])
 def test_w4a16_gemm_valu_variant_matches_oracle(M, K, N):

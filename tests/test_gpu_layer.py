@@ -34,9 +34,10 @@ def _oracle_dims(cfg):
 
 def gpu_stages(L_dev, src, kc, vc):
     """Every stage of the layer through the standalone entry points, each fed
-    the given stage inputs src (host fp16 bits: x, xn, qkv, o, h, hn, m);
-    the attention runs on fresh device copies of the caches kc, vc.  Returns
-    the stage outputs and the device caches."""
+    the given stage inputs src (host fp16 bits: x, qkv, o, h, m); the
+    attention runs on fresh device copies of the caches kc, vc.  The norms
+    run with the projections that read them (RMSNorm + QKV, RMSNorm +
+    SwiGLU).  Returns the stage outputs and the device caches."""
     cfg, s = L_dev.cfg, L_dev.cfg.shape
     T, H, F, Hd = cfg.T, s.H, s.F, s.Hq * s.D
     nb = max(ss.gemm_workspace_bytes(T, K, N) for _, K, N in s.gemms())
@@ -45,23 +46,21 @@ def gpu_stages(L_dev, src, kc, vc):
     ws = ss.workspace(nb, dev())
     new = lambda n: torch.zeros((T, n), dtype=torch.int16, device=dev())
     d = {k: up(v) for k, v in src.items()}
-    g = {k: new(n) for k, n in (("xn", H), ("qkv", s.n_qkv), ("o", Hd), ("h", H), ("hn", H),
-                                ("m", F), ("out", H))}
+    g = {k: new(n) for k, n in (("qkv", s.n_qkv), ("o", Hd), ("h", H), ("m", F), ("out", H))}
     dkc, dvc = up(kc), up(vc)
-    ss.rmsnorm(d["x"], L_dev.attn_norm, g["xn"])
-    ss.w4a16_gemm(L_dev.w4["wqkv"], d["xn"], g["qkv"], ws)
+    ss.rmsnorm_w4a16_gemm(L_dev.w4["wqkv"], d["x"], L_dev.attn_norm, g["qkv"], ws)
     q, k, v = _split_qkv(s, d["qkv"])
     ss.tree_attention(q, k, v, dkc, dvc, L_dev.P, L_dev.parent, s.Hq, s.Hkv, s.D, L_dev.rope, g["o"], ws)
     ss.w4a16_gemm(L_dev.w4["wo"], d["o"], g["h"], ws, residual=d["x"])
-    ss.rmsnorm(d["h"], L_dev.mlp_norm, g["hn"])
-    ss.w4a16_swiglu(L_dev.w4["wgate"], L_dev.w4["wup"], d["hn"], g["m"], ws)
+    ss.rmsnorm_w4a16_swiglu(L_dev.w4["wgate"], L_dev.w4["wup"], d["h"], L_dev.mlp_norm, g["m"], ws)
     ss.w4a16_gemm(L_dev.w4["wdown"], d["m"], g["out"], ws, residual=d["h"])
     torch.cuda.synchronize()
     assert ss.read_device_error(ws) == 0
     return {k: down16(t) for k, t in g.items()}, down16(dkc), down16(dvc)
 
 
-STAGES = ("xn", "qkv", "o", "h", "hn", "m", "out")
+STAGES = ("qkv", "o", "h", "m", "out")
+INPUTS = ("x", "qkv", "o", "h", "m")
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
@@ -83,7 +82,7 @@ def test_verify_layer_and_commit_match_oracle(name):
     # 1. the fused layer is exactly the composition of the standalone
     #    kernels: each entry point fed the layer's own stage inputs
     #    reproduces the layer's stage output bit for bit (GPU against GPU)
-    comp, ck, cv = gpu_stages(L_dev, {k: mid[k] for k in ("x", "xn", "qkv", "o", "h", "hn", "m")}, kc, vc)
+    comp, ck, cv = gpu_stages(L_dev, {k: mid[k] for k in INPUTS}, kc, vc)
     for k in STAGES:
         assert np.array_equal(comp[k], mid[k]), f"{name}: fused layer differs from the standalone {k} stage"
     assert np.array_equal(ck, gk) and np.array_equal(cv, gv)
@@ -91,7 +90,7 @@ def test_verify_layer_and_commit_match_oracle(name):
     #    fed the REFERENCE stage inputs, against the reference stage output
     okc, ovc = kc.copy(), vc.copy()
     ref = oracle_stages(cfg, w, okc, ovc, x, parent)
-    got, rk, rv = gpu_stages(L_dev, {k: ref[k] for k in ("x", "xn", "qkv", "o", "h", "hn", "m")}, kc, vc)
+    got, rk, rv = gpu_stages(L_dev, {k: ref[k] for k in INPUTS}, kc, vc)
     for k in STAGES:
         err, rel = check_close(got[k], ref[k], f"{name} stage {k}")
         print(f"{name} stage {k}: max abs err {err:.3g}, max rel err (|r|>=0.2) {rel:.3g}")

@@ -255,6 +255,14 @@ def time_ops(ctx, it, ss, torch, stream, dev):
     ops["attention"] = {"us": round(att_us, 3), "bytes": att_bytes}
     rn_us = time_op(lambda i: ss.rmsnorm(xin, inst[0]["an"], y[:, :s.H], stream=stream), it)
     ops["rmsnorm"] = {"us": round(rn_us, 3), "bytes": 2 * T * s.H * 2 + s.H * 2}
+    # the norm with the projection that reads it, as the layer runs them (in
+    # one kernel where the GEMM plan splits K within workgroups)
+    nq_us = time_op(lambda i: ss.rmsnorm_w4a16_gemm(inst[i % copies]["w4"]["wqkv"], xin, inst[0]["an"],
+                                                    y[:, :s.n_qkv], op_ws, stream=stream), it)
+    ops["rmsnorm_qkv"] = {"us": round(nq_us, 3), "bytes": w4b(s.H, s.n_qkv) + T * s.H * 2 + s.H * 2}
+    ns_us = time_op(lambda i: ss.rmsnorm_w4a16_swiglu(inst[i % copies]["w4"]["wgate"], inst[i % copies]["w4"]["wup"],
+                                                      xin, inst[0]["an"], y[:, :s.F], op_ws, stream=stream), it)
+    ops["rmsnorm_swiglu"] = {"us": round(ns_us, 3), "bytes": 2 * w4b(s.H, s.F) + T * s.H * 2 + s.H * 2}
     for k, v in ops.items():
         v["GBps"] = round(v["bytes"] / (v["us"] * 1e-6) / 1e9, 1)
         v["frac_hbm"] = round(v["GBps"] / HBM_PEAK_GBS, 4)

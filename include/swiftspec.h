@@ -171,13 +171,12 @@ int swiftspec_rmsnorm(const uint16_t* x, int32_t M, int32_t H, int32_t ldx, cons
  *   swiftspec_rmsnorm_w4a16_gemm  : y = fp16( xn . W'^T )
  *   swiftspec_rmsnorm_w4a16_swiglu: y = fp16( silu(xn . Wg'^T) * (xn . Wu'^T) )
  * with xn[m] = x[m] / sqrt(mean_k x[m][k]^2 + eps) * gamma over the K
- * columns.  Where the GEMM's plan gives each workgroup all of K (up to 16
- * rows, SwiGLU up to 8; K <= 8192; matrices of at most 32 MB) the norm
- * runs inside it:
- * the matrix-core operand is fp16(x * gamma) and row m of the fp32 product
- * is scaled by 1 / sqrt(mean x[m]^2 + eps) before the epilogue; otherwise
- * xn is formed in fp16 (as swiftspec_rmsnorm) and multiplied.  Both are
- * within the GEMM tolerance of the fp64 definition.  x [M][ldx], gamma [K]
+ * columns, xn rounded to fp16 (as swiftspec_rmsnorm computes it) and then
+ * multiplied.  Where the GEMM's plan gives each workgroup all of K and each
+ * of its waves at most 4 groups of 128 (up to 16 rows, SwiGLU up to 8;
+ * matrices of at most 32 MB) the norm runs inside the GEMM, which sums the
+ * rows' squares first and forms the fp16 operand values the same way;
+ * otherwise the norm kernel writes them for the GEMM.  x [M][ldx], gamma [K]
  * fp16, 16-byte aligned, ldx % 8 == 0; no residual; the workspace of
  * swiftspec_w4a16_gemm_workspace_bytes / _swiglu_workspace_bytes.  Other
  * arguments and errors as swiftspec_w4a16_gemm / _swiglu. */
@@ -464,9 +463,10 @@ typedef struct {
  *   xn = rmsnorm(x, attn_norm); qkv = xn.Wqkv'^T; o = tree_attention(qkv)
  *   h = x + o.Wo'^T; hn = rmsnorm(h, mlp_norm); m = silu(hn.Wg'^T) * (hn.Wu'^T)
  *   out = h + m.Wd'^T
- * with fp16 storage of qkv, o, h, m, out; the norms run with the
- * projections that read them (swiftspec_rmsnorm_w4a16_gemm / _swiglu), so
- * xn and hn are stored only where those form them in fp16.  The layer is
+ * with fp16 storage of xn, qkv, o, h, hn, m, out (xn and hn as the operand
+ * values of the projections that read them, swiftspec_rmsnorm_w4a16_gemm
+ * and _swiglu, which keep them in the workspace only where the norm runs
+ * as a kernel of its own).  The layer is
  * exactly the composition rmsnorm_w4a16_gemm, tree_attention, w4a16_gemm
  * (+ residual), rmsnorm_w4a16_swiglu, w4a16_gemm (+ residual).  hidden
  * [T][H] is read as x and overwritten with out.  The caches receive the tree's keys and values

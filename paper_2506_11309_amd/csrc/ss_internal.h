@@ -14,7 +14,7 @@ struct GemmLaunch {
   int K, N;       // N = output columns
   const uint16_t* aprep;  // activations in the prepared layout
   int M;
-  // non-null (K-split plans only, ksw > 0): the input is RMSNorm(xnorm)
+  // non-null (plans with norm_in_kslice only): the input is RMSNorm(xnorm)
   // with weight gamma [K], computed in the GEMM; aprep is not read
   const uint16_t* xnorm = nullptr;
   int ldx = 0;
@@ -33,8 +33,9 @@ struct GemmLaunch {
   float* part;  // split-K partial slots (2 per workgroup)
 };
 
-// Widest K whose RMSNorm a K-split GEMM applies itself (gamma staged in LDS).
-constexpr int kNormMaxK = 8192;
+// A K-split GEMM applies the RMSNorm of its input itself where no wave
+// holds more than this many 128-wide groups (all its loads in registers).
+constexpr int kNormMaxGroupsPerWave = 4;
 
 struct GemmPlan {
   int nw, nblocks, nwg, ksw = 0;
@@ -42,6 +43,7 @@ struct GemmPlan {
   size_t prep_bytes;  // prepared activations of the input
 };
 GemmPlan plan_w4a16_gemm(int M, int K, int N, bool swiglu);
+bool norm_in_kslice(const GemmPlan& p, int K);
 void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st);
 void launch_prepare_activations(const uint16_t* x, int M, int ldx, int K, uint16_t* out, hipStream_t st);
 void launch_prepack_w4(const uint8_t* q, const uint16_t* s, const uint8_t* z, int K, int N, void* packed,

@@ -78,7 +78,7 @@ struct NormIn {
 };
 
 bool norm_in_gemm(int M, const swiftspec_w4* W0, bool swiglu) {
-  return W0->K <= ss::kNormMaxK && ss::plan_w4a16_gemm(M, W0->K, W0->N, swiglu).ksw > 0;
+  return ss::norm_in_kslice(ss::plan_w4a16_gemm(M, W0->K, W0->N, swiglu), W0->K);
 }
 
 void run_gemm(const swiftspec_w4* W0, const swiftspec_w4* W1, const uint16_t* aprep, int M,

@@ -545,31 +545,12 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
 // and no second kernel runs.  Every workgroup reads the whole activation
 // matrix (from L2): four times the weight bytes, which is why the plan
 // keeps it to small weights.
-//
-// NORM: the input is the RMSNorm of plain rows x (Sec. 2's decoder layer
-// normalises the residual stream before the QKV and the FFN projections).
-// Since the workgroup reads all of K anyway, it normalises on the way: the
-// MFMA operand is fp16(x * gamma) (the 32 consecutive values a lane holds
-// are the 32 the prepared layout gives it, permuted in registers), each
-// lane accumulates its rows' sum of squares of x in fp32, and the epilogue
-// multiplies row m by 1 / sqrt(sum_k x^2 / K + eps): the same product with
-// the row scale applied after the contraction instead of before the fp16
-// rounding of the operand.  Each wave stages the gamma of its own groups in
-// LDS (K <= kNormMaxK; no barrier, the wave alone reads them), keeping the
-// register ring (and the occupancy) of the plain kernel; rows at or past M
-// lie outside the buffer range of x and load as zeros, without a branch.
-// The rows of a load sit at one stride (often a multiple of 4 KB), so
-// lanes reading the same 16-byte position of their rows collide in the
-// vector cache: load f of row r takes the 16-byte chunk f ^ (r & 3) and
-// two rounds of lane selects put the chunks back in order (measured on the
-// 1B-shaped QKV, 8 rows: 6.0 -> 5.1 us; 8B-shaped, 16 rows: 19.0 -> 13.5).
-template <int W, int NT, bool NORM>
+
+template <int W, int NT>
 __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   constexpr int kR = 3;
   static_assert(NT == 1 || NT == 2, "plain, or fused SwiGLU (gate and up tile of one column tile)");
   __shared__ f32x4 red[W][NT][kWave];
-  __shared__ float red_ss[NORM ? W : 1][16];
-  __shared__ u32x4 gam[NORM ? kNormMaxK / 8 : 1];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int ncol = lane & 15, kq = lane >> 4;
@@ -580,27 +561,8 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   const auto rq0 = buffer_rsrc(a.w0.q, q_bytes), rs0 = buffer_rsrc(a.w0.sz, sz_bytes);
   const auto rq1 = buffer_rsrc(NT == 2 ? a.w1.q : a.w0.q, q_bytes);
   const auto rs1 = buffer_rsrc(NT == 2 ? a.w1.sz : a.w0.sz, sz_bytes);
-  const auto ra = NORM ? buffer_rsrc(a.x, (uint32_t)((size_t)a.M * a.ldx * 2))
-                      : buffer_rsrc(a.a, (uint32_t)(G * 4 * kWave * 16));
-  // gamma over this wave's groups only: chunks past them load as zeros
-  const auto rgm = buffer_rsrc(NORM ? a.gamma + g0 * 128 : a.a, (uint32_t)(n * 256));
-  // NORM: the 16-byte chunks of gamma over this wave's groups (16 per
-  // group; at most kNormMaxK / 128 / W groups), loaded before the ring's
-  // first loads and written to LDS after them
-  constexpr int kGamPer = NORM ? (kNormMaxK / 128 / W * 16 + kWave - 1) / kWave : 1;
-  u32x4 gtmp[kGamPer];
-  if constexpr (NORM) {
-#pragma unroll
-    for (int j = 0; j < kGamPer; ++j) {
-      gtmp[j] = buffer_load_x4(rgm, (uint32_t)(lane + j * kWave) * 16u, 0);
-    }
-  }
+  const auto ra = buffer_rsrc(a.a, (uint32_t)(G * 4 * kWave * 16));
   const uint32_t lane16 = (uint32_t)lane * 16u, col4 = (uint32_t)ncol * 4u;
-  // NORM: byte offset of this lane's 32 values k = 128 g + 32 kq + t of row
-  // ncol (g = 0), and of the same 32 values of gamma
-  const uint32_t xrow = (uint32_t)((ncol * a.ldx + 32 * kq) * 2);
-  const int xsw = ncol & 3;  // NORM: load f takes chunk f ^ xsw
-  const uint32_t xm1 = 0u - (uint32_t)(xsw & 1), xm2 = 0u - (uint32_t)(xsw >> 1);
   struct Stage {
     u32x4 b[NT];
     uint32_t sz[NT];
@@ -615,12 +577,9 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
       st.b[nt] = buffer_load_x4(nt ? rq1 : rq0, lane16, tg * 1024u);
       st.sz[nt] = buffer_load_x1(nt ? rs1 : rs0, col4, tg * 64u);
     }
-    if constexpr (NORM) {
-#pragma unroll
-      for (int f = 0; f < 4; ++f) st.x[f] = buffer_load_x4(ra, xrow + (uint32_t)((f ^ xsw) * 16), (uint32_t)(g * 256));
-    } else if (ncol < a.M) {
-      // lanes of rows at or past M load nothing (zeros in the prepared
-      // layout; the MFMA rows they feed are not written)
+    // lanes of rows at or past M load nothing (zeros in the prepared
+    // layout; the MFMA rows they feed are not written)
+    if (ncol < a.M) {
 #pragma unroll
       for (int f = 0; f < 4; ++f) st.x[f] = buffer_load_x4(ra, lane16, (uint32_t)((g * 4 + f) * 1024));
     }
@@ -630,20 +589,9 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   f32x4 acc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float ssq = 0.f;
   Stage ring[kR];
 #pragma unroll
   for (int j = 0; j < kR - 1; ++j) load(ring[j], j);
-  if constexpr (NORM) {
-#pragma unroll
-    for (int j = 0; j < kGamPer; ++j) {
-      const int c = lane + j * kWave;
-      if (c < n * 16) gam[g0 * 16 + c] = gtmp[j];
-    }
-    // a wave's LDS accesses complete in issue order: its reads below see
-    // these writes; only the compiler has to keep the order
-    asm volatile("" ::: "memory");
-  }
   for (int i0 = 0; i0 < n; i0 += kR) {
 #pragma unroll
     for (int J = 0; J < kR; ++J) {
@@ -651,37 +599,7 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
       load(ring[(J + kR - 1) % kR], i + kR - 1);
       const Stage& st = ring[J];
       if (i < n) {
-        u32x4 xa[4];
-        if constexpr (NORM) {
-          u32x4 gm[4];
-#pragma unroll
-          for (int f = 0; f < 4; ++f) gm[f] = gam[(g0 + i) * 16 + kq * 4 + f];
-          // chunk c is in load c ^ xsw: bitwise selects under the masks
-          // m1, m2 (a conditional operator here becomes an indexed copy
-          // through scratch memory)
-          u32x4 t1[4], xc[4];
-#pragma unroll
-          for (int c = 0; c < 4; ++c)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) t1[c][e] = (st.x[c ^ 1][e] & xm1) | (st.x[c][e] & ~xm1);
-#pragma unroll
-          for (int c = 0; c < 4; ++c)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) xc[c][e] = (t1[c ^ 2][e] & xm2) | (t1[c][e] & ~xm2);
-          uint32_t w[16];
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const half2v xv = bitcast<half2v>(xc[q][e]);
-              ssq = __builtin_amdgcn_fdot2(xv, xv, ssq, false);
-              w[4 * q + e] = bitcast<uint32_t>(xv * bitcast<half2v>(gm[q][e]));
-            }
-          pack_prepared(w, xa);
-        } else {
-#pragma unroll
-          for (int f = 0; f < 4; ++f) xa[f] = st.x[f];
-        }
+        const u32x4* xa = st.x;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const BFrag bf = dequant_block(st.b[nt], st.sz[nt], magic_lo, magic_hi);
@@ -705,12 +623,6 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
   }
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) red[wave][nt][lane] = acc[nt];
-  if constexpr (NORM) {
-    // row ncol's sum over the wave's groups: add the four kq lanes
-    ssq += __shfl_xor(ssq, 16, kWave);
-    ssq += __shfl_xor(ssq, 32, kWave);
-    if (kq == 0) red_ss[wave][ncol] = ssq;
-  }
   __syncthreads();
   if (wave != 0) return;
   f32x4 sum[NT];
@@ -720,17 +632,172 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
 #pragma unroll
     for (int w = 1; w < W; ++w) sum[nt] += red[w][nt][lane];
   }
-  if constexpr (NORM) {
+  const int col = t * 16 + ncol;
+  const int G2 = a.N >> 7;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 4 * kq + r;
-      float tot = red_ss[0][m];
-#pragma unroll
-      for (int w = 1; w < W; ++w) tot += red_ss[w][m];
-      const float inv = 1.0f / sqrtf(tot / (float)a.K + a.eps);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) sum[nt][r] *= inv;
+  for (int r = 0; r < 4; ++r) {
+    const int m = 4 * kq + r;
+    if (m < a.M) {
+      float val;
+      if constexpr (NT == 2) {
+        const float gte = sum[0][r];
+        val = gte / (1.0f + __expf(-gte)) * sum[1][r];
+      } else {
+        val = sum[0][r] + (a.res ? h2f(a.res[(size_t)m * a.ldr + col]) : 0.f);
+      }
+      const uint16_t h = f2h(val);
+      if (a.y) a.y[(size_t)m * a.ldy + col] = h;
+      if (a.yp) store_prepared(a.yp, m, col, G2, h);
     }
+  }
+}
+
+
+// ------------------------------------------- small M, RMSNorm in the GEMM
+// The QKV projection and the fused SwiGLU read the RMSNorm of the residual
+// stream (the decoder layer of Sec. 2).  Where the K-split plan gives each
+// wave at most NG (2 or 4) groups, the workgroup (which reads all of K
+// anyway) normalises the plain rows x itself: every wave issues all its
+// loads up front (gamma of its groups, then per group the weight blocks and
+// the row chunks), sums x^2 over its groups, the waves' sums meet in LDS,
+// and each lane forms its operand values exactly as the norm kernel does,
+// fp16((x * inv) * gamma) in fp32, inv = 1 / sqrt(sum_k x^2 / K + eps), so
+// the operand is rounded where the unfused chain rounds it.  Rows at or
+// past M lie outside the buffer range of x and load as zeros, without a
+// branch.  The rows of one load sit at one stride (often a multiple of
+// 4 KB), and lanes reading the same 16-byte position of their rows collide
+// in the vector cache (a row stride of 4 KB + 16 B was 0.8 us faster on the
+// 1B-shaped QKV, one of 4 KB + 128 B no faster): load f of row r takes the
+// 16-byte chunk f ^ (r & 3) and two rounds of bitwise lane selects put the
+// chunks back in order.
+template <int W, int NT, int NG>
+__global__ __launch_bounds__(64 * W) void w4a16_kslice_norm_kernel(GemmArgs a) {
+  static_assert(NT == 1 || NT == 2, "plain, or fused SwiGLU (gate and up tile of one column tile)");
+  static_assert(NG == 2 || NG == 4, "groups per wave");
+  __shared__ f32x4 red[W][NT][kWave];
+  __shared__ float red_ss[W][16];
+  __shared__ u32x4 gam[W][kWave];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int ncol = lane & 15, kq = lane >> 4;
+  const int t = blockIdx.x;
+  const int G = a.G;
+  const int g0 = wave * G / W, n = (wave + 1) * G / W - g0;  // 1 .. NG: the plan keeps W <= G <= NG W
+  const uint32_t q_bytes = (uint32_t)((size_t)a.K * a.N / 2), sz_bytes = (uint32_t)((size_t)a.N * G * 4);
+  const auto rq0 = buffer_rsrc(a.w0.q, q_bytes), rs0 = buffer_rsrc(a.w0.sz, sz_bytes);
+  const auto rq1 = buffer_rsrc(NT == 2 ? a.w1.q : a.w0.q, q_bytes);
+  const auto rs1 = buffer_rsrc(NT == 2 ? a.w1.sz : a.w0.sz, sz_bytes);
+  const auto rx = buffer_rsrc(a.x, (uint32_t)((size_t)a.M * a.ldx * 2));
+  // gamma over this wave's groups only (chunk c = 16 j + 4 kq + f of group
+  // g0 + j); chunks past them load as zeros
+  const auto rgm = buffer_rsrc(a.gamma + g0 * 128, (uint32_t)(n * 256));
+  const uint32_t lane16 = (uint32_t)lane * 16u, col4 = (uint32_t)ncol * 4u;
+  // this lane's 32 values k = 128 g + 32 kq + t of row ncol, at g = 0
+  const uint32_t xrow = (uint32_t)((ncol * a.ldx + 32 * kq) * 2);
+  const int xsw = ncol & 3;  // load f takes chunk f ^ xsw
+  const uint32_t xm1 = 0u - (uint32_t)(xsw & 1), xm2 = 0u - (uint32_t)(xsw >> 1);
+
+  const u32x4 gv = buffer_load_x4(rgm, lane16, 0);
+  u32x4 b[NG][NT], x[NG][4];
+  uint32_t sz[NG][NT];
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    const int g = g0 + (j < n ? j : n - 1);  // past the range: repeat the last group, unused
+    const uint32_t tg = (uint32_t)(t * G + g);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      b[j][nt] = buffer_load_x4(nt ? rq1 : rq0, lane16, tg * 1024u);
+      sz[j][nt] = buffer_load_x1(nt ? rs1 : rs0, col4, tg * 64u);
+    }
+#pragma unroll
+    for (int f = 0; f < 4; ++f) x[j][f] = buffer_load_x4(rx, xrow + (uint32_t)((f ^ xsw) * 16), (uint32_t)(g * 256));
+  }
+  gam[wave][lane] = gv;
+
+  // chunk c is in load c ^ xsw: bitwise selects under the masks xm1, xm2 (a
+  // conditional operator here becomes an indexed copy through scratch
+  // memory); then this wave's part of each row's sum of squares
+  float ssq = 0.f;
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    u32x4 t1[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t1[c][e] = (x[j][c ^ 1][e] & xm1) | (x[j][c][e] & ~xm1);
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[j][c][e] = (t1[c ^ 2][e] & xm2) | (t1[c][e] & ~xm2);
+    if (j < n) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const half2v v = bitcast<half2v>(x[j][c][e]);
+          ssq = __builtin_amdgcn_fdot2(v, v, ssq, false);
+        }
+    }
+  }
+  ssq += __shfl_xor(ssq, 16, kWave);
+  ssq += __shfl_xor(ssq, 32, kWave);
+  if (kq == 0) red_ss[wave][ncol] = ssq;
+  __syncthreads();
+  float tot = red_ss[0][ncol];
+#pragma unroll
+  for (int w = 1; w < W; ++w) tot += red_ss[w][ncol];
+  const float inv = 1.0f / sqrtf(tot / (float)a.K + a.eps);
+
+  uint32_t magic_lo = 0x64006400u, magic_hi = 0x54005400u;
+  asm volatile("" : "+v"(magic_lo), "+v"(magic_hi));
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    if (j < n) {
+      uint32_t w[16];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const u32x4 gm = gam[wave][16 * j + 4 * kq + c];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          // (x * inv) * gamma, each product rounded to fp32, then to fp16:
+          // fused multiply-adds of +0 are those products (up to the sign
+          // of an exact zero) and take the fp16 operands directly
+          const half2v v = bitcast<half2v>(x[j][c][e]), gg = bitcast<half2v>(gm[e]);
+          half2v o;
+          o[0] = (_Float16)__builtin_fmaf(__builtin_fmaf((float)v[0], inv, 0.f), (float)gg[0], 0.f);
+          o[1] = (_Float16)__builtin_fmaf(__builtin_fmaf((float)v[1], inv, 0.f), (float)gg[1], 0.f);
+          w[4 * c + e] = bitcast<uint32_t>(o);
+        }
+      }
+      u32x4 xa[4];
+      pack_prepared(w, xa);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const BFrag bf = dequant_block(b[j][nt], sz[j][nt], magic_lo, magic_hi);
+        f32x4 cc = {0.f, 0.f, 0.f, 0.f};
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(xa[0]), bf.lo_a, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(xa[1]), bf.lo_b, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(xa[2]), bf.hi_a, cc, 0, 0, 0);
+        cc = __builtin_amdgcn_mfma_f32_16x16x32_f16(bitcast<half8>(xa[3]), bf.hi_b, cc, 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          acc[nt][r] = __builtin_fmaf(cc[r], (float)bitcast<half2v>(sz[j][nt])[0], acc[nt][r]);
+      }
+    }
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) red[wave][nt][lane] = acc[nt];
+  __syncthreads();
+  if (wave != 0) return;
+  f32x4 sum[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    sum[nt] = red[0][nt][lane];
+#pragma unroll
+    for (int w = 1; w < W; ++w) sum[nt] += red[w][nt][lane];
   }
   const int col = t * 16 + ncol;
   const int G2 = a.N >> 7;
@@ -888,8 +955,7 @@ static void launch_mt(const GemmLaunch& L, hipStream_t st) {
   }
 }
 
-template <int W, int NT, bool NORM>
-static void launch_kslice(const GemmLaunch& L, hipStream_t st) {
+static GemmArgs kslice_args(const GemmLaunch& L) {
   GemmArgs a = {};
   auto unpack = [&](const void* p) {
     return W4Ptr{reinterpret_cast<const u32x4*>(p),
@@ -911,19 +977,36 @@ static void launch_kslice(const GemmLaunch& L, hipStream_t st) {
   a.ldx = L.ldx;
   a.gamma = L.gamma;
   a.eps = L.eps;
-  hipLaunchKernelGGL((w4a16_kslice_kernel<W, NT, NORM>), dim3(L.N / 16), dim3(64 * W), 0, st, a);
+  return a;
+}
+
+template <int W, int NT>
+static void launch_kslice(const GemmLaunch& L, hipStream_t st) {
+  hipLaunchKernelGGL((w4a16_kslice_kernel<W, NT>), dim3(L.N / 16), dim3(64 * W), 0, st, kslice_args(L));
+}
+
+template <int W, int NT, int NG>
+static void launch_kslice_norm(const GemmLaunch& L, hipStream_t st) {
+  hipLaunchKernelGGL((w4a16_kslice_norm_kernel<W, NT, NG>), dim3(L.N / 16), dim3(64 * W), 0, st, kslice_args(L));
+}
+
+bool norm_in_kslice(const GemmPlan& p, int K) {
+  return p.ksw > 0 && (K / 128 + p.ksw - 1) / p.ksw <= kNormMaxGroupsPerWave;
 }
 
 void launch_w4a16_gemm(const GemmLaunch& L, hipStream_t st) {
+  // K-split plans give the fused SwiGLU 4 waves, plain GEMMs 4 or 8
+  if (L.ksw && L.xnorm) {
+    const bool two = (L.K / 128 + L.ksw - 1) / L.ksw <= 2;  // groups per wave (norm_in_kslice: <= 4)
+    if (L.swiglu) two ? launch_kslice_norm<4, 2, 2>(L, st) : launch_kslice_norm<4, 2, 4>(L, st);
+    else if (L.ksw == 8) two ? launch_kslice_norm<8, 1, 2>(L, st) : launch_kslice_norm<8, 1, 4>(L, st);
+    else two ? launch_kslice_norm<4, 1, 2>(L, st) : launch_kslice_norm<4, 1, 4>(L, st);
+    return;
+  }
   if (L.ksw) {
-    const bool nrm = L.xnorm != nullptr;
-    if (L.swiglu) {
-      if (L.ksw == 8) nrm ? launch_kslice<8, 2, true>(L, st) : launch_kslice<8, 2, false>(L, st);
-      else nrm ? launch_kslice<4, 2, true>(L, st) : launch_kslice<4, 2, false>(L, st);
-    } else {
-      if (L.ksw == 8) nrm ? launch_kslice<8, 1, true>(L, st) : launch_kslice<8, 1, false>(L, st);
-      else nrm ? launch_kslice<4, 1, true>(L, st) : launch_kslice<4, 1, false>(L, st);
-    }
+    if (L.swiglu) launch_kslice<4, 2>(L, st);
+    else if (L.ksw == 8) launch_kslice<8, 1>(L, st);
+    else launch_kslice<4, 1>(L, st);
     return;
   }
   if (L.swiglu) launch_mt<EPI_SWIGLU>(L, st);

@@ -351,22 +351,25 @@ def test_w4a16_swiglu_two_column_blocks(M, K, N):
 
 
 @pytest.mark.parametrize("M,K,N,ldx,swiglu", [
-    (8, 2048, 3072, 2048, False), (1, 2048, 3072, 2048, False), (7, 8192, 2560, 8192, False),
+    # norm inside the K-split GEMM: 2 groups per wave, then up to 4
+    (8, 2048, 3072, 2048, False), (1, 2048, 3072, 2048, False), (6, 1024, 2048, 1032, False),
     (8, 1152, 2048, 1280, False), (5, 1920, 2048, 1920, False), (13, 4096, 6144, 4096, False),
-    (16, 1152, 2048, 1288, False), (16, 4096, 4096, 4096, False),  # norm inside the K-split GEMM
-    (3, 16384, 2048, 16384, False),                                # K past the in-GEMM limit
+    (16, 1152, 2048, 1288, False), (16, 4096, 4096, 4096, False),
+    # norm kernel, then the K-split GEMM (8 and 16 groups per wave)
+    (7, 8192, 2560, 8192, False), (3, 16384, 2048, 16384, False),
     (17, 2048, 3072, 2048, False), (32, 8192, 1024, 8200, False),  # norm kernel, then stream-K
-    (8, 2048, 8192, 2048, True), (3, 1920, 4096, 2056, True),      # inside the K-split SwiGLU
+    (4, 1024, 2048, 1024, True), (8, 2048, 8192, 2048, True), (3, 1920, 4096, 2056, True),  # in the SwiGLU
     (9, 2048, 8192, 2048, True)])                                  # norm kernel, then the SwiGLU
 def test_rmsnorm_then_projection_matches_oracle(M, K, N, ldx, swiglu):
     """RMSNorm followed by the QKV-style projection or the fused SwiGLU,
     against the reference's fp16 rmsnorm then its fp64 product: where each
-    workgroup holds all of K the norm runs inside the GEMM (operand x *
-    gamma, row scale after the contraction, each row's 16-byte chunks
-    loaded in a row-dependent order), else as its own kernel; both within
-    the GEMM tolerance, with strided rows (ldx > K, also not a multiple of
-    16 bytes apart), ragged M and unequal K ranges per wave (K = 1152,
-    1920); two calls agree bit for bit."""
+    workgroup holds all of K and each wave at most 4 groups the norm runs
+    inside the GEMM (row sums first, then the operand normalised as the
+    norm kernel does it; each row's 16-byte chunks loaded in a
+    row-dependent order), else as its own kernel; both within the GEMM
+    tolerance, with strided rows (ldx > K, also not a multiple of 16 bytes
+    apart), ragged M and unequal K ranges per wave (K = 1152, 1920); two
+    calls agree bit for bit."""
     seed = 50 + M + K % 1000
     x = gen.normal_f16(seed, 0, (M, ldx), 0.0, 2.0)
     gamma = gen.normal_f16(seed, 1, (K,), 1.0, 0.2)
@@ -393,6 +396,22 @@ def test_rmsnorm_then_projection_matches_oracle(M, K, N, ldx, swiglu):
         outs.append(down16(dy))
     assert np.array_equal(outs[0], outs[1])
     check_close(outs[0], ref, f"rmsnorm then {'swiglu' if swiglu else 'gemm'} M={M} K={K} N={N}")
+    # the normalised operand is rounded where the two-kernel chain rounds it
+    # (fp16 of (x * inv) * gamma): against the norm kernel followed by the
+    # plain entry point the outputs differ only through the last bits of
+    # inv (an fp16 ulp of a rare normalised value, or of an output), far
+    # inside what rounding x * gamma instead would produce
+    xn_d = torch.zeros((M, K), dtype=torch.int16, device=dev())
+    ss.rmsnorm(dx[:, :K], dg, xn_d)
+    dy = torch.zeros((M, N), dtype=torch.int16, device=dev())
+    if swiglu:
+        ss.w4a16_swiglu(d, du, xn_d, dy, ws)
+    else:
+        ss.w4a16_gemm(d, xn_d, dy, ws)
+    torch.cuda.synchronize()
+    chain = down16(dy).view(np.float16).astype(np.float64)
+    diff = np.abs(outs[0].view(np.float16).astype(np.float64) - chain)
+    assert np.all(diff <= 5e-4 + 1e-3 * np.abs(chain)), diff.max()
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 1024, 1024), (8, 2048, 512), (13, 1024, 2048), (32, 8192, 1024),

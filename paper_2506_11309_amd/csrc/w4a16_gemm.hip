@@ -485,7 +485,12 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
   constexpr int kBatch = 8;
   constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;
   constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;
-  const int nb = blockIdx.x;
+  // the GEMM orders its ranges XCD-major (workgroup b on XCD b % 8 takes
+  // range (b % 8) nwg/8 + b / 8), so the blocks of XCD x are the x-th eighth
+  // of all blocks: fix-up workgroup b takes one of those of its own XCD,
+  // whose partials that XCD's L2 wrote
+  const int b = blockIdx.x;
+  const int nb = (a.nwg % 8 == 0 && a.nblocks % 8 == 0) ? (b % 8) * (a.nblocks / 8) + b / 8 : b;
   const long U = a.units;
   const int G = a.G;
   const int c_first = (int)((((long)nb * G + 1) * a.nwg - 1) / U);

@@ -181,17 +181,21 @@ def test_tp4_shard_gemms(name, K, N, res):
     print(f"tp4 {name} (M 8, K {K}, N {N}): max abs err {err:.3g}, rel {rel:.3g}")
 
 
-def test_tp4_shard_swiglu_with_fixup():
-    """M = 8, K = 8192, N = 7168: 112 column blocks of 64, fewer than the
-    compute units, so the blocks are split between workgroups and the fix-up
-    kernel sums the gate and up partials in order before silu(g) * u."""
-    M, K, N = 8, 8192, 7168
+@pytest.mark.parametrize("M", [8, 12])
+def test_tp4_shard_swiglu(M):
+    """K = 8192, N = 7168.  M = 8 (the shard's batch): one workgroup per
+    16-column tile, gate and up tile together, K split across 4 waves.
+    M = 12 (past the K-split SwiGLU's 8 rows): 112 column blocks of 64,
+    fewer than the compute units, so stream-K splits them between
+    workgroups and the fix-up kernel sums the gate and up partials in order
+    before silu(g) * u."""
+    K, N = 8192, 7168
     Wg, Wu = _w4(350, N, K), _w4(351, N, K)
-    x = gen.normal_f16(352, 0, (M, K))
+    x = gen.normal_f16(352, M, (M, K))
     outs = [_swiglu(Wg, Wu, x) for _ in range(2)]
     assert np.array_equal(outs[0], outs[1])
-    err, rel = check_close(outs[0], oracle.w4a16_swiglu(Wg, Wu, x), "tp4 swiglu")
-    print(f"tp4 swiglu (M 8, K 8192, N 7168): max abs err {err:.3g}, rel {rel:.3g}")
+    err, rel = check_close(outs[0], oracle.w4a16_swiglu(Wg, Wu, x), f"tp4 swiglu M={M}")
+    print(f"tp4 swiglu (M {M}, K 8192, N 7168): max abs err {err:.3g}, rel {rel:.3g}")
 
 
 @pytest.mark.parametrize("P", [500, 1000, 4096])

@@ -140,7 +140,8 @@ struct Epilogue {
   static constexpr int kColB = 4 * kColW;
   float rv[MT][kColW][4];
 
-  __device__ __forceinline__ void load_residual(const GemmArgs& a, int nb, int wave, int lane) {
+  // rows m0 + 16 mt + ... (m0: first row of the caller's M-tiles)
+  __device__ __forceinline__ void load_residual(const GemmArgs& a, int nb, int wave, int lane, int m0 = 0) {
     const int ncol = lane & 15, kq = lane >> 4;
     const int col0 = (nb * kColB + wave * kColW) * 16;
 #pragma unroll
@@ -157,14 +158,14 @@ struct Epilogue {
         for (int ct = 0; ct < kColW; ++ct)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int m = mt * 16 + kq * 4 + r;
+            const int m = m0 + mt * 16 + kq * 4 + r;
             rv[mt][ct][r] = h2f(a.res[(size_t)(m < a.M ? m : 0) * a.ldr + col0 + ct * 16 + ncol]);
           }
     }
   }
 
   __device__ __forceinline__ void write(const GemmArgs& a, int nb, int wave, int lane,
-                                        const f32x4 (&acc)[MT][NWV]) const {
+                                        const f32x4 (&acc)[MT][NWV], int m0 = 0) const {
     const int ncol = lane & 15, kq = lane >> 4;
     const int col0 = (nb * kColB + wave * kColW) * 16;
     const int G2 = a.N >> 7;
@@ -175,7 +176,7 @@ struct Epilogue {
         const int ncl = col0 + ct * 16 + ncol;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int m = mt * 16 + kq * 4 + r;
+          const int m = m0 + mt * 16 + kq * 4 + r;
           if (m < a.M) {
             float val;
             if (EPI == EPI_SWIGLU) {
@@ -477,19 +478,26 @@ void w4a16_gemm_kernel(GemmArgs a) {
   }
 }
 
-// Split N-blocks: one workgroup per N-block sums the partials of its
-// contributing ranges in workgroup order (deterministic) and writes the
-// outputs; N-blocks inside one range were written by the GEMM kernel.
+// Split N-blocks: one workgroup per M-tile of an N-block (grid MT times the
+// N-blocks) sums that tile's partials of the block's contributing ranges in
+// workgroup order (deterministic) and writes its 16 rows; N-blocks inside
+// one range were written by the GEMM kernel.  (One workgroup for all M-tiles
+// of a block was slower: at 32 rows 20.4 -> 19.1 us for the 70B QKV, 35.3
+// -> 34.1 us for the down projection; at 64 rows 51.4 -> 48.6 us for the
+// down projection, whose one-workgroup form needs 256 VGPRs.)
 template <int MT, int NWV, int EPI>
 __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
+  constexpr int MS = 1;  // M-tiles per workgroup
   constexpr int kBatch = 8;
   constexpr int kColW = (EPI == EPI_SWIGLU) ? NWV / 2 : NWV;
   constexpr int kSrc = (EPI == EPI_SWIGLU) ? 2 : 1;
   // the GEMM orders its ranges XCD-major (workgroup b on XCD b % 8 takes
   // range (b % 8) nwg/8 + b / 8), so the blocks of XCD x are the x-th eighth
-  // of all blocks: fix-up workgroup b takes one of those of its own XCD,
+  // of all blocks: fix-up workgroup (b, M-tile group) takes one of those of
+  // its own XCD (b % 8, the grid holding MT copies of the blocks),
   // whose partials that XCD's L2 wrote
-  const int b = blockIdx.x;
+  const int b = blockIdx.x % a.nblocks;
+  const int mt0 = blockIdx.x / a.nblocks;  // this workgroup's M-tile
   const int nb = (a.nwg % 8 == 0 && a.nblocks % 8 == 0) ? (b % 8) * (a.nblocks / 8) + b / 8 : b;
   const long U = a.units;
   const int G = a.G;
@@ -498,25 +506,25 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
   if (c_first == c_last) return;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
-  Epilogue<MT, NWV, EPI> ep;
-  ep.load_residual(a, nb, wave, lane);  // in flight with the first partial loads
-  f32x4 acc[MT][NWV];
+  Epilogue<MS, NWV, EPI> ep;
+  ep.load_residual(a, nb, wave, lane, mt0 * 16);  // in flight with the first partial loads
+  f32x4 acc[MS][NWV];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int mt = 0; mt < MS; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NWV; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int c0 = c_first; c0 <= c_last; c0 += kBatch) {
     // kBatch contributors' loads in flight at once, summed in order
-    f32x4 pa[kBatch][MT][kColW], pb[kBatch][MT][kColW];
+    f32x4 pa[kBatch][MS][kColW], pb[kBatch][MS][kColW];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int c = c0 + j <= c_last ? c0 + j : c_last;
       const float* src = part_slot<MT, NWV, EPI>(a, c, nb == (int)(range_begin(U, c, a.nwg) / G) ? 0 : 1, wave);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MS; ++mt)
 #pragma unroll
         for (int ct = 0; ct < kColW; ++ct) {
-          const int t = mt * kColW + ct;
+          const int t = (mt0 + mt) * kColW + ct;
           pa[j][mt][ct] = *reinterpret_cast<const f32x4*>(src + ((size_t)(t * kSrc) * kWave + lane) * 4);
           if (EPI == EPI_SWIGLU) pb[j][mt][ct] = *reinterpret_cast<const f32x4*>(src + ((size_t)(t * kSrc + 1) * kWave + lane) * 4);
         }
@@ -525,7 +533,7 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
     for (int j = 0; j < kBatch; ++j) {
       if (c0 + j > c_last) break;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MS; ++mt)
 #pragma unroll
         for (int ct = 0; ct < kColW; ++ct) {
           acc[mt][ct] += pa[j][mt][ct];
@@ -533,7 +541,7 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
         }
     }
   }
-  ep.write(a, nb, wave, lane, acc);
+  ep.write(a, nb, wave, lane, acc, mt0 * 16);
 }
 
 // ------------------------------------------------- small M, small weights
@@ -923,8 +931,9 @@ static void launch_t(const GemmLaunch& L, hipStream_t st) {
   // ranges split no N-block when every workgroup gets whole N-blocks (the
   // split SwiGLU is only planned that way)
   if constexpr (EPI != EPI_SWIGLU_SPLIT) {
-    if (L.nblocks % L.nwg != 0)
-      hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks), dim3(256), 0, st, a);
+    if (L.nblocks % L.nwg != 0) {
+      hipLaunchKernelGGL((w4a16_fixup_kernel<MT, NW, EPI>), dim3(L.nblocks * MT), dim3(256), 0, st, a);
+    }
   }
 }
 

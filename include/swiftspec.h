@@ -101,7 +101,9 @@ int swiftspec_read_device_error(void* ws, void* stream, uint32_t* out);
  *            (scale | zero << 16) per (column, group).  The compute entry
  *            points read only `packed`; qweight/scales/zeros are needed only
  *            by swiftspec_w4_prepack.
- * K % 128 == 0, N % 64 == 0 (four waves of 16 output columns). */
+ * K % 128 == 0, N % 64 == 0 (four waves of 16 output columns), and the
+ * kernel-native copy below 4 GiB (swiftspec_w4_packed_bytes(K, N) <= 2^32 - 1;
+ * UNSUPPORTED otherwise). */
 typedef struct {
   const uint8_t* qweight;
   const uint16_t* scales;

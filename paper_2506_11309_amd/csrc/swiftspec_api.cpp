@@ -43,6 +43,8 @@ int check_w4_shape(const swiftspec_w4* W) {
   if (!W) return SWIFTSPEC_INVALID_ARG;
   if (W->K <= 0 || W->N <= 0) return SWIFTSPEC_INVALID_ARG;
   if (W->K % 128 != 0 || W->N % 64 != 0) return SWIFTSPEC_UNSUPPORTED;
+  // the kernels address the packed matrix through 32-bit buffer ranges
+  if (ss::w4_packed_bytes(W->K, W->N) > 0xFFFFFFFFull) return SWIFTSPEC_UNSUPPORTED;
   return SWIFTSPEC_OK;
 }
 

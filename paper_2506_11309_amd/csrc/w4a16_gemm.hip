@@ -71,11 +71,15 @@ struct GemmArgs {
   const uint16_t* res;
   int ldr;
   int nblocks, nwg;
-  long units;
+  uint32_t units;  // N-blocks x groups; units x nwg < 2^30 (K N / 2 < 2^32)
   float* part;
 };
 
-__device__ __forceinline__ long range_begin(long units, int v, int nwg) { return units * v / nwg; }
+// first unit of workgroup v's range (32-bit: units x nwg stays below 2^30
+// because a packed matrix fits a 32-bit buffer range)
+__device__ __forceinline__ int range_begin(uint32_t units, int v, int nwg) {
+  return (int)((units * (uint32_t)v) / (uint32_t)nwg);
+}
 
 template <int MT, int NWV>
 struct BStage {
@@ -226,7 +230,7 @@ void w4a16_gemm_kernel(GemmArgs a) {
   const int G = a.G;
   const int b = blockIdx.x;
   const int v = (a.nwg % 8 == 0) ? (b % 8) * (a.nwg / 8) + b / 8 : b;
-  const int u_lo = (int)range_begin(a.units, v, a.nwg), u_hi = (int)range_begin(a.units, v + 1, a.nwg);
+  const int u_lo = range_begin(a.units, v, a.nwg), u_hi = range_begin(a.units, v + 1, a.nwg);
   const int total = u_hi - u_lo;
   if (total <= 0) return;
 
@@ -499,11 +503,14 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
   const int b = blockIdx.x % a.nblocks;
   const int mt0 = blockIdx.x / a.nblocks;  // this workgroup's M-tile
   const int nb = (a.nwg % 8 == 0 && a.nblocks % 8 == 0) ? (b % 8) * (a.nblocks / 8) + b / 8 : b;
-  const long U = a.units;
-  const int G = a.G;
-  const int c_first = (int)((((long)nb * G + 1) * a.nwg - 1) / U);
-  const int c_last = (int)((((long)nb * G + G) * a.nwg - 1) / U);
+  const uint32_t U = a.units, lo = (uint32_t)(nb * a.G), nwg = (uint32_t)a.nwg;
+  const int c_first = (int)(((lo + 1) * nwg - 1) / U);
+  const int c_last = (int)(((lo + (uint32_t)a.G) * nwg - 1) / U);
   if (c_first == c_last) return;
+  // every contributor after the first begins its range inside this block
+  // (slot 0, its first block); the first one holds it in slot 1 (its last
+  // block) unless its range begins exactly at the block
+  const int slot_first = range_begin(U, c_first, a.nwg) < (int)lo ? 1 : 0;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   Epilogue<MS, NWV, EPI> ep;
@@ -519,7 +526,7 @@ __global__ __launch_bounds__(256) void w4a16_fixup_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int c = c0 + j <= c_last ? c0 + j : c_last;
-      const float* src = part_slot<MT, NWV, EPI>(a, c, nb == (int)(range_begin(U, c, a.nwg) / G) ? 0 : 1, wave);
+      const float* src = part_slot<MT, NWV, EPI>(a, c, c == c_first ? slot_first : 0, wave);
 #pragma unroll
       for (int mt = 0; mt < MS; ++mt)
 #pragma unroll
@@ -925,7 +932,7 @@ static void launch_t(const GemmLaunch& L, hipStream_t st) {
   a.ldr = L.ldr;
   a.nblocks = L.nblocks;
   a.nwg = L.nwg;
-  a.units = (long)L.nblocks * a.G;
+  a.units = (uint32_t)(L.nblocks * a.G);
   a.part = L.part;
   hipLaunchKernelGGL((w4a16_gemm_kernel<MT, NW, EPI>), dim3(L.nwg), dim3(256), 0, st, a);
   // ranges split no N-block when every workgroup gets whole N-blocks (the

@@ -61,6 +61,15 @@ def test_host_side_validation_rejects_before_launch(ss):
     # too many rows
     assert lib.swiftspec_w4a16_gemm(ctypes.byref(W), fake, 65, 4096, fake, 1024, None, 0, fake, 1 << 30,
                                     None) == ss.UNSUPPORTED
+    # a kernel-native copy of 4 GiB or more (past the kernels' 32-bit buffer ranges)
+    W_huge = ss.W4(fake, fake, fake, 131072, 65536, fake)
+    assert lib.swiftspec_w4_packed_bytes(131072, 65536) > 0xFFFFFFFF
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W_huge), fake, 8, 131072, fake, 65536, None, 0, fake, 1 << 40,
+                                    None) == ss.UNSUPPORTED
+    W_edge = ss.W4(fake, fake, fake, 65536, 65536, fake)  # 2 GiB + scales: accepted by the shape check
+    assert lib.swiftspec_w4_packed_bytes(65536, 65536) < 0xFFFFFFFF
+    assert lib.swiftspec_w4a16_gemm(ctypes.byref(W_edge), fake, 8, 65536, fake, 65536, None, 0, fake, 16,
+                                    None) == ss.WORKSPACE_TOO_SMALL
     # misaligned activations / leading dimension
     assert lib.swiftspec_w4a16_gemm(ctypes.byref(W), fake + 2, 8, 4096, fake, 1024, None, 0, fake, 1 << 30,
                                     None) == ss.MISALIGNED

@@ -717,20 +717,26 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_norm_kernel(GemmArgs a) {
   const int xsw = ncol & 3;  // load f takes chunk f ^ xsw
   const uint32_t xm1 = 0u - (uint32_t)(xsw & 1), xm2 = 0u - (uint32_t)(xsw >> 1);
 
-  const u32x4 gv = buffer_load_x4(rgm, lane16, 0);
+  // the row chunks first, then gamma, then the weights: the row sums wait
+  // for the first loads only, while the weight blocks are still in flight
   u32x4 b[NG][NT], x[NG][4];
   uint32_t sz[NG][NT];
 #pragma unroll
   for (int j = 0; j < NG; ++j) {
     const int g = g0 + (j < n ? j : n - 1);  // past the range: repeat the last group, unused
+#pragma unroll
+    for (int f = 0; f < 4; ++f) x[j][f] = buffer_load_x4(rx, xrow + (uint32_t)((f ^ xsw) * 16), (uint32_t)(g * 256));
+  }
+  const u32x4 gv = buffer_load_x4(rgm, lane16, 0);
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    const int g = g0 + (j < n ? j : n - 1);
     const uint32_t tg = (uint32_t)(t * G + g);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       b[j][nt] = buffer_load_x4(nt ? rq1 : rq0, lane16, tg * 1024u);
       sz[j][nt] = buffer_load_x1(nt ? rs1 : rs0, col4, tg * 64u);
     }
-#pragma unroll
-    for (int f = 0; f < 4; ++f) x[j][f] = buffer_load_x4(rx, xrow + (uint32_t)((f ^ xsw) * 16), (uint32_t)(g * 256));
   }
   gam[wave][lane] = gv;
 

@@ -25,6 +25,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -67,10 +68,16 @@ SHAPE_LABEL = {2048: "Llama-3.2-1B", 4096: "Llama-3-8B", 8192: "Llama-3-70B"}
 
 
 def source_hash(paths):
+    """Hash of the code of C++/HIP sources: comments dropped and white space
+    collapsed, so an edited comment keeps the hash and any code change alters
+    it (the hashed sources hold no string literal with a comment marker)."""
     h = hashlib.sha256()
     for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

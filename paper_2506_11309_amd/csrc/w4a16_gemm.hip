@@ -679,9 +679,8 @@ __global__ __launch_bounds__(64 * W) void w4a16_kslice_kernel(GemmArgs a) {
 // wave at most NG (2 or 4) groups, the workgroup (which reads all of K
 // anyway) normalises the plain rows x itself: every wave issues all its
 // loads up front (the row chunks of its groups, gamma, then the weight
-// blocks, so that the row sums wait for the row chunks only; this order was
-// 5.5 us faster on the 8B-shaped layer at 64 rows), sums x^2 over its
-// groups, the waves' sums meet in LDS,
+// blocks, so that the row sums wait for the row chunks only), sums x^2
+// over its groups, the waves' sums meet in LDS,
 // and each lane forms its operand values exactly as the norm kernel does,
 // fp16((x * inv) * gamma) in fp32, inv = 1 / sqrt(sum_k x^2 / K + eps), so
 // the operand is rounded where the unfused chain rounds it.  Rows at or

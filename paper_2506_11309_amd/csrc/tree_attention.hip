@@ -843,8 +843,12 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W * TPW 
             if (!ok) s[t2][h][r] = -INFINITY;
           }
       }
-      lm[t2] = fmaxf(fmaxf(fmaxf(s[t2][0][0], s[t2][0][1]), fmaxf(s[t2][0][2], s[t2][0][3])),
-                     fmaxf(fmaxf(s[t2][1][0], s[t2][1][1]), fmaxf(s[t2][1][2], s[t2][1][3])));
+      // (IEEE maximum: three-input v_maximum3_f32, where fmaxf would add
+      // one quieting v_max per matrix-core result; a NaN score makes its
+      // probability NaN either way)
+      auto mx = [](float x, float y) { return __builtin_elementwise_maximum(x, y); };
+      lm[t2] = mx(mx(mx(s[t2][0][0], s[t2][0][1]), mx(s[t2][0][2], s[t2][0][3])),
+                  mx(mx(s[t2][1][0], s[t2][1][1]), mx(s[t2][1][2], s[t2][1][3])));
     }
     // move a row's reference up only when one of its scores exceeds it by
     // more than 2^8 (the probabilities then stay below 256), and set it at
